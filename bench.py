@@ -1,0 +1,227 @@
+#!/usr/bin/env python3
+"""SpMM benchmark: GNN aggregation Y = A.X with per-layer format selection.
+
+One step = one GNN layer's aggregation through the selector
+(gs_select_and_run) on one batch of features, with the adjacency's features,
+prediction and format conversion already cached from the warm-up (the paper
+decides the format once per layer across epochs, Sec. 5.2); those first-call
+costs are measured and reported separately.  Steps rotate over several
+(X, Y) batches so that consecutive steps do not find their operands in the
+256 MiB last-level cache.
+
+Headline workload: the power-law graph (n = 100,000, Chung-Lu exponent 2.1,
+mean degree 10, GCN-normalised fp32, X 100,000 x 128 fp32).  Also reported:
+every format's SpMM time on the same workload, the selector's speedup over
+fixed CSR, the roofline fraction of the dominant kernel, and the CPU oracle's
+throughput on this machine's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
+
+WORKLOADS = {
+    1: "tiny ER GCN n=2048 F=64",
+    2: "power-law Chung-Lu n=100000 gamma=2.1 deg=10 GCN F=128",
+    3: "mesh 512x512 5-point n=262144 F=64",
+    4: "block-community n=204800 (16-node blocks p=0.8, 2 inter/node) GCN F=256",
+    5: "large Chung-Lu n=2000000 gamma=2.0 deg=25 row-stochastic F=128 (layer 1)",
+}
+
+
+def b_alg(R, C, Z, F):
+    """Algorithmic bytes of one SpMM: CSR-equivalent A, X read once, Y written once."""
+    return 4 * (R + 1) + 8 * Z + 4 * C * F + 4 * R * F
+
+
+def time_launches(fn, stream, reps, inputs):
+    """Per-launch durations (s) of fn(i) measured with HIP events on `stream`."""
+    import torch
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for i in range(reps):
+        ev[i][0].record(stream)
+        fn(inputs[i % len(inputs)])
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    return np.array([a.elapsed_time(b) * 1e-3 for a, b in ev])
+
+
+def cpu_baseline(g, F, budget_s=10.0):
+    import oracle
+
+    rp = oracle.csr(g.R, g.row)
+    X = g.X[:, :F]
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        oracle.spmm(g.R, rp, g.col, g.val, X)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    flops = 2.0 * g.nnz * F * reps
+    return {
+        "value": round(flops / el / 1e9, 3),
+        "unit": "GFLOP/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": f"full {g.R}-row SpMM (fp64 accumulation, plus |A||X|) repeated {reps}x in {el:.1f}s",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default: power-law)")
+    ap.add_argument("--batches", type=int, default=4, help="rotating (X, Y) batches")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-budget", type=float, default=10.0)
+    ap.add_argument("--format-reps", type=int, default=50)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on one GPU only (no multi-GPU path); use --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import graphgen
+    import paper_2111_00352_amd as gs
+
+    assert torch.cuda.is_available(), "bench needs a GPU"
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream()
+
+    t_gen = time.perf_counter()
+    g = graphgen.config(args.config)
+    t_gen = time.perf_counter() - t_gen
+    R, C, Z, F = g.R, g.C, g.nnz, g.F
+    row = torch.from_numpy(g.row).to(dev)
+    col = torch.from_numpy(g.col).to(dev)
+    val = torch.from_numpy(g.val).to(dev)
+    Xs, Ys = [], []
+    rng = np.random.default_rng(7)
+    for b in range(args.batches):
+        X = torch.from_numpy(g.X if b == 0 else rng.permutation(g.X, axis=0)).to(dev)
+        Xs.append(X)
+        Ys.append(torch.empty((R, F), dtype=torch.float32, device=dev))
+    torch.cuda.synchronize()
+
+    flops = 2.0 * Z * F
+    balg = b_alg(R, C, Z, F)
+
+    # ---- selector: first call (features + prediction + conversion), then steady state
+    ctx = gs.SelectContext("model")
+    t0 = time.perf_counter()
+    _, chosen = ctx.run(1, row, col, val, (R, C), Xs[0], out=Ys[0])
+    torch.cuda.synchronize()
+    first_call_s = time.perf_counter() - t0
+    st = ctx.stats()
+
+    def step(i):
+        return ctx.run(1, row, col, val, (R, C), Xs[i % args.batches], out=Ys[i % args.batches])
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    ms_per_step = el / args.steps * 1e3
+    value = flops / (el / args.steps) / 1e9
+
+    # ---- per-launch duration of the chosen format's SpMM (HIP events on its stream)
+    mats = {}
+    fmt_rows = {}
+    for fmt in ("csr", "coo", "ell", "dia", "bsr"):
+        try:
+            t0 = time.perf_counter()
+            m = gs.build_format(row, col, val, (R, C), fmt)
+            torch.cuda.synchronize()
+            t_build = time.perf_counter() - t0
+        except gs.GnnSpmmError as e:
+            fmt_rows[fmt] = {"feasible": False, "bytes_required": getattr(e, "bytes_required", None)}
+            continue
+        mats[fmt] = m
+        pairs = list(zip(Xs, Ys))
+        for i in range(3):
+            m.spmm(*pairs[i % len(pairs)][:1], out=pairs[i % len(pairs)][1])
+        d = time_launches(lambda p: m.spmm(p[0], out=p[1]), stream, args.format_reps, pairs)
+        t = float(np.median(d))
+        fmt_rows[fmt] = {
+            "feasible": True, "median_us": round(t * 1e6, 2), "min_us": round(float(d.min()) * 1e6, 2),
+            "gflops": round(flops / t / 1e9, 1), "roofline_frac": round(balg / t / 1e9 / HBM_PEAK_GBS, 4),
+            "format_bytes": m.device_bytes, "build_s": round(t_build, 4),
+        }
+    d_sel = time_launches(lambda p: ctx.run(1, row, col, val, (R, C), p[0], out=p[1]), stream,
+                          args.format_reps, list(zip(Xs, Ys)))
+    t_sel = float(np.median(d_sel))
+    feasible = {k: v for k, v in fmt_rows.items() if v.get("feasible")}
+    best = min(feasible, key=lambda k: feasible[k]["median_us"])
+    t_csr = feasible["csr"]["median_us"]
+    achieved = balg / t_sel / 1e9
+
+    out = {
+        "metric": "SpMM GFLOP/s (2*nnz*F) + % HBM roofline per format; best-vs-CSR speedup",
+        "value": round(value, 2),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": WORKLOADS[args.config], "n": R, "nnz": Z, "F": F,
+                   "batches": args.batches},
+        "roofline": {
+            "bound": "hbm",
+            "kernel": f"spmm_{chosen} (all launches of one SpMM)",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "bytes_per_launch": balg,
+            "launch_us": round(t_sel * 1e6, 2),
+        },
+        "selector": {
+            "mode": "model",
+            "chosen": chosen,
+            "best_measured": best,
+            "speedup_vs_csr": round(t_csr / (t_sel * 1e6), 3),
+            "best_vs_csr": round(t_csr / feasible[best]["median_us"], 3),
+            "first_call_s": round(first_call_s, 4),
+            "t_features_s": round(st["t_features"], 4),
+            "t_convert_s": round(st["t_convert"], 4),
+        },
+        "formats": fmt_rows,
+        "gen_s": round(t_gen, 2),
+        "device": torch.cuda.get_device_name(0),
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(g, F, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,201 @@
+// Internal declarations of the gfx950 SpMM library: matrix handle layout,
+// allocation, error reporting and the kernel launchers shared between files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/gnnspmm.h"
+
+namespace gs {
+
+// ----------------------------------------------------------------- errors
+
+void set_error(const char *fmt, ...) __attribute__((format(printf, 1, 2)));
+
+struct Error {
+    int code;
+};
+
+// Throws Error{GS_ERR_HIP} with the HIP message when e != hipSuccess.
+void hip_check(hipError_t e, const char *what);
+#define GS_HIP(call) ::gs::hip_check((call), #call)
+
+[[noreturn]] void fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+
+// Runs f, converting Error / std::bad_alloc into status codes.
+template <class Fn>
+int guarded(Fn &&f)
+{
+    try {
+        f();
+        return GS_OK;
+    } catch (const Error &e) {
+        return e.code;
+    } catch (const std::bad_alloc &) {
+        set_error("host allocation failed");
+        return GS_ERR_OOM;
+    } catch (...) {
+        set_error("unexpected internal exception");
+        return GS_ERR_INVALID_ARG;
+    }
+}
+
+// --------------------------------------------------------------- memory
+
+void *dev_alloc(size_t bytes, hipStream_t s);  // throws Error{GS_ERR_OOM}
+void dev_free(void *p, hipStream_t s);
+
+// A device buffer freed when the owner goes away.
+struct DevBuf {
+    void *p = nullptr;
+    size_t bytes = 0;
+    hipStream_t s = nullptr;
+    DevBuf() = default;
+    DevBuf(const DevBuf &) = delete;
+    DevBuf &operator=(const DevBuf &) = delete;
+    DevBuf(DevBuf &&o) noexcept : p(o.p), bytes(o.bytes), s(o.s) { o.p = nullptr; o.bytes = 0; }
+    DevBuf &operator=(DevBuf &&o) noexcept
+    {
+        if (this != &o) {
+            reset();
+            p = o.p; bytes = o.bytes; s = o.s;
+            o.p = nullptr; o.bytes = 0;
+        }
+        return *this;
+    }
+    ~DevBuf() { reset(); }
+    void alloc(size_t n, hipStream_t st)
+    {
+        reset();
+        s = st;
+        bytes = n;
+        p = n ? dev_alloc(n, st) : nullptr;
+    }
+    void reset()
+    {
+        if (p) dev_free(p, s);
+        p = nullptr;
+        bytes = 0;
+    }
+    template <class T> T *as() const { return static_cast<T *>(p); }
+};
+
+// ------------------------------------------------------------ matrix handle
+
+}  // namespace gs
+
+struct gs_matrix_ {
+    int fmt = GS_CSR;
+    int64_t R = 0, C = 0, Z = 0;
+    hipStream_t stream = nullptr;  // stream the arrays were allocated on
+
+    // COO (row, col, val) and CSR (row_ptr, col, val) share col/val.
+    gs::DevBuf row, row_ptr, col, val;
+    // ELL
+    int64_t K = 0;
+    gs::DevBuf ell_col, ell_val;
+    // DIA
+    int64_t ND = 0;
+    gs::DevBuf offsets, dia;
+    // BSR
+    int32_t b = 0;
+    int64_t nb = 0;
+    gs::DevBuf bptr, bcol, bval, bmask;  // bmask: per block 64-bit mask of nonzero columns
+    int64_t n_dense_blocks = 0;
+
+    // Kernel plans built once per matrix.
+    // CSR: rows longer than the short-row limit, split into chunks.
+    int csr_long_thr = 0, csr_chunk = 0, coo_chunk = 0;
+    int64_t n_long_rows = 0, n_long_chunks = 0;
+    gs::DevBuf long_rows;    // int32 row ids, n_long_rows
+    gs::DevBuf long_chunk;   // int32 [n_long_chunks] -> index into long_rows
+    gs::DevBuf long_first;   // int32 [n_long_rows+1] -> first chunk of each long row
+    // COO: rows with no entries (zeroed by the COO kernel)
+    int64_t n_empty_rows = 0;
+    gs::DevBuf empty_rows;
+
+    // F-dependent workspace (partials / carries), grown on demand.
+    gs::DevBuf work;
+
+    uint64_t device_bytes = 0;
+};
+
+namespace gs {
+
+constexpr uint64_t kDefaultMaxBytes = 8ull << 30;
+constexpr int kDefaultBsrBlock = 16;
+
+// Rows longer than this go through the split (multi-workgroup) CSR path.
+constexpr int kCsrLongRow = 256;
+// Chunk length of the split CSR path and of the COO segmented reduction.
+constexpr int kCsrChunk = 256;
+constexpr int kCooChunk = 256;
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// ----------------------------------------------------------- scan (gs_scan)
+
+// Exclusive prefix sum of n int32 values (in may equal out).  out[n] is also
+// written with the total when out_has_total.  Enqueued on s.
+void exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, bool out_has_total,
+                        hipStream_t s);
+
+// ------------------------------------------------------ build (gs_build)
+
+struct CanonCOO {
+    int64_t R = 0, C = 0, Z = 0;
+    DevBuf row, col, val;     // canonical order (owned)
+};
+
+// Validates A and produces its canonical COO.  Throws Error on invalid input.
+void canonicalize(const gs_coo &A, bool assume_canonical, hipStream_t s, CanonCOO &out);
+
+// Builds a CSR handle from canonical COO (takes ownership of col/val).
+gs_matrix_ *csr_from_canon(CanonCOO &&c, hipStream_t s);
+
+// Builds format fmt from a CSR handle (not consumed).
+gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint64_t max_bytes,
+                             hipStream_t s, uint64_t *bytes_required);
+
+// Canonical COO arrays of any handle into caller memory.
+void to_coo(const gs_matrix_ &m, int32_t *row, int32_t *col, float *val, hipStream_t s);
+
+// Builds a CSR handle from any handle (via its canonical COO).
+gs_matrix_ *csr_from_any(const gs_matrix_ &m, hipStream_t s);
+
+// Bytes a format would need for this CSR (from the features' aggregates).
+uint64_t format_bytes(int fmt, int64_t R, int64_t C, int64_t Z, int64_t K, int64_t ND,
+                      int64_t nb, int b);
+
+// Counts distinct (row/b, col/b) blocks of a CSR matrix (device, synchronises).
+int64_t count_blocks(const gs_matrix_ &csr, int b, hipStream_t s);
+
+// --------------------------------------------------- features (gs_features)
+
+void features_from_csr(const gs_matrix_ &csr, hipStream_t s, gs_features *out);
+
+// ------------------------------------------------------- spmm (gs_spmm_*)
+
+void spmm_csr(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+              hipStream_t s);
+void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+              hipStream_t s);
+void spmm_ell(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+              hipStream_t s);
+void spmm_dia(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+              hipStream_t s);
+void spmm_bsr(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+              hipStream_t s);
+
+// Plans built at conversion time for the CSR and COO kernels.
+void plan_csr(gs_matrix_ &m, hipStream_t s);
+void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s);
+
+// Makes sure m.work holds at least bytes (reallocating in stream order).
+void ensure_work(gs_matrix_ &m, size_t bytes, hipStream_t s);
+
+}  // namespace gs

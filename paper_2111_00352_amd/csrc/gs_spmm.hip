@@ -1,0 +1,664 @@
+// SpMM Y = A.X for each storage format (the aggregation of a GNN layer,
+// Sec. 2.1; formats of Sec. 2.2).  fp32 in and out, fused multiply-add.
+//
+// Shared layout of every kernel: a "row group" of G lanes (G in {8,16,32,64},
+// always inside one 64-wide wavefront) owns one output row slice of G*VEC
+// columns, lane l holding columns l*VEC .. l*VEC+VEC-1 as one vector; X rows
+// are gathered with one VEC-wide load per lane, so a group reads G*VEC*4
+// contiguous bytes of an X row per nonzero (256 B at F = 64 up to 1 KiB at
+// F = 256).  grid.y walks F in slices of G*VEC columns when F is wider.
+// Index/value streams are read once and are loaded cooperatively by the
+// group (one entry per lane) and broadcast with cross-lane shuffles.
+//
+// Every sequential fp32 chain is bounded (row chunks of at most 256 terms,
+// four interleaved accumulators), which keeps the rounding error far below
+// 1e-5 |A||X|; partial sums of split rows are combined in a fixed order, so
+// results are deterministic.
+#include <cstdlib>
+#include <cstring>
+#include <vector>
+
+#include "gs_device.h"
+#include "gs_internal.h"
+
+namespace gs {
+namespace {
+
+constexpr int kBlock = 256;  // threads per workgroup for every SpMM kernel
+
+template <int VEC>
+struct Acc {
+    float v[VEC];
+    __device__ __forceinline__ void zero()
+    {
+#pragma unroll
+        for (int i = 0; i < VEC; i++) v[i] = 0.0f;
+    }
+    __device__ __forceinline__ void fma(float a, const Vec<VEC> &x)
+    {
+#pragma unroll
+        for (int i = 0; i < VEC; i++) v[i] = __builtin_fmaf(a, x.v[i], v[i]);
+    }
+    __device__ __forceinline__ void add(const Acc &o)
+    {
+#pragma unroll
+        for (int i = 0; i < VEC; i++) v[i] += o.v[i];
+    }
+    __device__ __forceinline__ Vec<VEC> vec() const
+    {
+        Vec<VEC> r;
+#pragma unroll
+        for (int i = 0; i < VEC; i++) r.v[i] = v[i];
+        return r;
+    }
+};
+
+// Accumulates sum_{k in [k0,k1)} val[k] * X[col[k], c0 .. c0+VEC) for one
+// group.  Entries are fetched G at a time (one per lane) and broadcast;
+// four independent accumulators keep four X-row loads in flight per lane.
+template <int VEC, int G>
+__device__ __forceinline__ Acc<VEC> gather_range(const int32_t *__restrict__ col,
+                                                 const float *__restrict__ val, int64_t k0,
+                                                 int64_t k1, const float *__restrict__ X,
+                                                 int64_t ldx, int64_t c0, bool active, int lane)
+{
+    Acc<VEC> a0, a1, a2, a3;
+    a0.zero();
+    a1.zero();
+    a2.zero();
+    a3.zero();
+    for (int64_t kb = k0; kb < k1; kb += G) {
+        const int64_t k = kb + lane;
+        int cj = 0;
+        float vj = 0.0f;
+        if (k < k1) {
+            cj = ld_stream(col + k);
+            vj = ld_stream(val + k);
+        }
+        const int n = (int)((k1 - kb) < G ? (k1 - kb) : G);
+        int j = 0;
+        for (; j + 4 <= n; j += 4) {
+            const int c_0 = __shfl(cj, j, G), c_1 = __shfl(cj, j + 1, G);
+            const int c_2 = __shfl(cj, j + 2, G), c_3 = __shfl(cj, j + 3, G);
+            const float v_0 = __shfl(vj, j, G), v_1 = __shfl(vj, j + 1, G);
+            const float v_2 = __shfl(vj, j + 2, G), v_3 = __shfl(vj, j + 3, G);
+            if (active) {
+                const Vec<VEC> x0 = ld_vec<VEC>(X + (int64_t)c_0 * ldx + c0);
+                const Vec<VEC> x1 = ld_vec<VEC>(X + (int64_t)c_1 * ldx + c0);
+                const Vec<VEC> x2 = ld_vec<VEC>(X + (int64_t)c_2 * ldx + c0);
+                const Vec<VEC> x3 = ld_vec<VEC>(X + (int64_t)c_3 * ldx + c0);
+                a0.fma(v_0, x0);
+                a1.fma(v_1, x1);
+                a2.fma(v_2, x2);
+                a3.fma(v_3, x3);
+            }
+        }
+        for (; j < n; j++) {
+            const int c_0 = __shfl(cj, j, G);
+            const float v_0 = __shfl(vj, j, G);
+            if (active) a0.fma(v_0, ld_vec<VEC>(X + (int64_t)c_0 * ldx + c0));
+        }
+    }
+    a0.add(a1);
+    a2.add(a3);
+    a0.add(a2);
+    return a0;
+}
+
+// ---------------------------------------------------------------- CSR
+// Blocks [0, n_row_tiles): one group per row for rows of at most long_thr
+// entries.  Blocks [n_row_tiles, ...): one group per chunk of a long row,
+// writing its partial sum to work[chunk * F + c].
+
+template <int VEC, int G>
+__global__ __launch_bounds__(kBlock) void k_csr_main(
+    int64_t R, const int32_t *__restrict__ rp, const int32_t *__restrict__ col,
+    const float *__restrict__ val, const float *__restrict__ X, int64_t ldx,
+    float *__restrict__ Y, int64_t ldy, int64_t F, int long_thr, int64_t n_row_tiles,
+    const int32_t *__restrict__ long_rows, const int32_t *__restrict__ long_chunk,
+    const int32_t *__restrict__ long_first, int64_t n_chunks, int chunk_len,
+    float *__restrict__ work)
+{
+    constexpr int GPB = kBlock / G;  // groups per block
+    const int g = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t c0 = (int64_t)blockIdx.y * (G * VEC) + (int64_t)lane * VEC;
+    const bool active = c0 < F;
+    const int64_t bid = blockIdx.x;
+    if (bid < n_row_tiles) {
+        const int64_t row = xcd_tile(bid, n_row_tiles) * GPB + g;
+        if (row >= R) return;
+        const int64_t s = rp[row], e = rp[row + 1];
+        if (e - s > long_thr) return;
+        Acc<VEC> acc = gather_range<VEC, G>(col, val, s, e, X, ldx, c0, active, lane);
+        if (active) st_vec_stream<VEC>(Y + row * ldy + c0, acc.vec());
+    } else {
+        const int64_t ch = (bid - n_row_tiles) * GPB + g;
+        if (ch >= n_chunks) return;
+        const int lr = long_chunk[ch];
+        const int64_t row = long_rows[lr];
+        const int64_t s = rp[row] + (ch - long_first[lr]) * (int64_t)chunk_len;
+        int64_t e = s + chunk_len;
+        if (e > rp[row + 1]) e = rp[row + 1];
+        Acc<VEC> acc = gather_range<VEC, G>(col, val, s, e, X, ldx, c0, active, lane);
+        if (active) st_vec<VEC>(work + ch * F + c0, acc.vec());
+    }
+}
+
+// One group per long row: sums its chunks' partials in chunk order.
+template <int VEC, int G>
+__global__ __launch_bounds__(kBlock) void k_csr_combine(const int32_t *__restrict__ long_rows,
+                                                        const int32_t *__restrict__ long_first,
+                                                        int64_t n_long, const float *__restrict__ work,
+                                                        float *__restrict__ Y, int64_t ldy, int64_t F)
+{
+    constexpr int GPB = kBlock / G;
+    const int g = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t c0 = (int64_t)blockIdx.y * (G * VEC) + (int64_t)lane * VEC;
+    const int64_t lr = (int64_t)blockIdx.x * GPB + g;
+    if (lr >= n_long || c0 >= F) return;
+    Acc<VEC> acc;
+    acc.zero();
+    for (int64_t ch = long_first[lr]; ch < long_first[lr + 1]; ch++) {
+        const Vec<VEC> p = ld_vec<VEC>(work + ch * F + c0);
+#pragma unroll
+        for (int i = 0; i < VEC; i++) acc.v[i] += p.v[i];
+    }
+    st_vec_stream<VEC>(Y + (int64_t)long_rows[lr] * ldy + c0, acc.vec());
+}
+
+// ---------------------------------------------------------------- COO
+// Segmented reduction over the (row, col)-sorted triplets.  Group q owns
+// entries [q*CH, (q+1)*CH).  Row boundaries inside the chunk are found with
+// a ballot over "row differs from the previous entry"; a segment is written
+// straight to Y unless its row continues into a neighbouring chunk, in which
+// case its partial goes to a carry slot: slot H (index 0) for the chunk's
+// first segment when that row began in an earlier chunk, slot T (index 1)
+// for the chunk's last segment when its row begins here and continues.
+// k_coo_fixup then adds each spanning row's carries in chunk order.
+
+template <int VEC>
+__device__ __forceinline__ void coo_flush(const Acc<VEC> &acc, int64_t row, bool first_seg,
+                                          bool last_seg, bool head_cont, bool tail_cont,
+                                          int64_t q, float *__restrict__ Y, int64_t ldy,
+                                          float *__restrict__ work, int64_t F, int64_t c0,
+                                          bool active)
+{
+    if (!active) return;
+    if (first_seg && head_cont)
+        st_vec<VEC>(work + (q * 2 + 0) * F + c0, acc.vec());
+    else if (last_seg && tail_cont)
+        st_vec<VEC>(work + (q * 2 + 1) * F + c0, acc.vec());
+    else
+        st_vec_stream<VEC>(Y + row * ldy + c0, acc.vec());
+}
+
+template <int VEC, int G>
+__global__ __launch_bounds__(kBlock) void k_coo_main(int64_t Z, const int32_t *__restrict__ row,
+                                                     const int32_t *__restrict__ col,
+                                                     const float *__restrict__ val,
+                                                     const float *__restrict__ X, int64_t ldx,
+                                                     float *__restrict__ Y, int64_t ldy, int64_t F,
+                                                     int chunk_len, int64_t n_chunks,
+                                                     float *__restrict__ work)
+{
+    constexpr int GPB = kBlock / G;
+    const int g = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t c0 = (int64_t)blockIdx.y * (G * VEC) + (int64_t)lane * VEC;
+    const bool active = c0 < F;
+    const int64_t q = xcd_tile(blockIdx.x, gridDim.x) * GPB + g;
+    if (q >= n_chunks) return;
+    const int64_t k0 = q * chunk_len;
+    const int64_t k1 = (k0 + chunk_len < Z) ? k0 + chunk_len : Z;
+    const bool head_cont = k0 > 0 && row[k0 - 1] == row[k0];
+    const bool tail_cont = k1 < Z && row[k1] == row[k1 - 1];
+    const int gbase = (threadIdx.x % kWave) / G * G;  // first lane of this group in the wave
+
+    Acc<VEC> acc;
+    acc.zero();
+    int64_t cur = row[k0];
+    bool first_seg = true;
+    for (int64_t kb = k0; kb < k1; kb += G) {
+        const int64_t k = kb + lane;
+        int rj = -1, cj = 0;
+        float vj = 0.0f;
+        if (k < k1) {
+            rj = ld_stream(row + k);
+            cj = ld_stream(col + k);
+            vj = ld_stream(val + k);
+        }
+        // bit j set: entry kb+j starts a new row relative to entry kb+j-1
+        const int rprev = __shfl(rj, lane == 0 ? 0 : lane - 1, G);
+        const bool starts = (k < k1) && lane > 0 && rj != rprev;
+        const unsigned long long heads =
+            (__ballot(starts) >> gbase) & (G == 64 ? ~0ull : ((1ull << G) - 1));
+        const int n = (int)((k1 - kb) < G ? (k1 - kb) : G);
+        for (int j = 0; j < n; j++) {
+            const int r_j = __shfl(rj, j, G);
+            const int c_j = __shfl(cj, j, G);
+            const float v_j = __shfl(vj, j, G);
+            if ((j == 0 && r_j != cur) || ((heads >> j) & 1ull)) {
+                // the row changes before entry j: flush the finished segment
+                coo_flush<VEC>(acc, cur, first_seg, false, head_cont, tail_cont, q, Y, ldy, work,
+                               F, c0, active);
+                first_seg = false;
+                acc.zero();
+                cur = r_j;
+            }
+            if (active) acc.fma(v_j, ld_vec<VEC>(X + (int64_t)c_j * ldx + c0));
+        }
+    }
+    coo_flush<VEC>(acc, cur, first_seg, true, head_cont, tail_cont, q, Y, ldy, work, F, c0,
+                   active);
+}
+
+// Groups [0, n_chunks): chunk q whose last segment starts a spanning row
+// adds that row's carries (slot T of q, then slot H of q+1, q+2, ... while
+// the row continues) and writes Y.  Groups after that zero the empty rows.
+template <int VEC, int G>
+__global__ __launch_bounds__(kBlock) void k_coo_fixup(int64_t Z, const int32_t *__restrict__ row,
+                                                      int chunk_len, int64_t n_chunks,
+                                                      const float *__restrict__ work,
+                                                      const int32_t *__restrict__ empty_rows,
+                                                      int64_t n_empty, float *__restrict__ Y,
+                                                      int64_t ldy, int64_t F)
+{
+    constexpr int GPB = kBlock / G;
+    const int g = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t c0 = (int64_t)blockIdx.y * (G * VEC) + (int64_t)lane * VEC;
+    const int64_t q = (int64_t)blockIdx.x * GPB + g;
+    if (c0 >= F) return;
+    if (q < n_chunks) {
+        const int64_t k0 = q * chunk_len;
+        const int64_t k1 = (k0 + chunk_len < Z) ? k0 + chunk_len : Z;
+        const bool tail_cont = k1 < Z && row[k1] == row[k1 - 1];
+        if (!tail_cont) return;
+        const bool head_cont = k0 > 0 && row[k0 - 1] == row[k0];
+        const int32_t r = row[k1 - 1];
+        if (head_cont && row[k0] == r) return;  // the row started in an earlier chunk
+        Acc<VEC> acc;
+        acc.zero();
+        const Vec<VEC> t = ld_vec<VEC>(work + (q * 2 + 1) * F + c0);
+#pragma unroll
+        for (int i = 0; i < VEC; i++) acc.v[i] = t.v[i];
+        for (int64_t p = q + 1; p < n_chunks; p++) {
+            const Vec<VEC> h = ld_vec<VEC>(work + (p * 2 + 0) * F + c0);
+#pragma unroll
+            for (int i = 0; i < VEC; i++) acc.v[i] += h.v[i];
+            const int64_t p0 = p * chunk_len;
+            const int64_t p1 = (p0 + chunk_len < Z) ? p0 + chunk_len : Z;
+            const bool whole = row[p1 - 1] == r && p1 < Z && row[p1] == r;
+            if (!whole) break;
+        }
+        st_vec_stream<VEC>(Y + (int64_t)r * ldy + c0, acc.vec());
+    } else {
+        const int64_t e = q - n_chunks;
+        if (e >= n_empty) return;
+        Vec<VEC> z;
+#pragma unroll
+        for (int i = 0; i < VEC; i++) z.v[i] = 0.0f;
+        st_vec_stream<VEC>(Y + (int64_t)empty_rows[e] * ldy + c0, z);
+    }
+}
+
+// ---------------------------------------------------------------- ELL
+// One group per row; slot (i,k) lives at k*R + i, so for a fixed k the
+// groups of a block read consecutive addresses.  Padding (col = -1) ends
+// the row (entries are packed to the front).
+
+template <int VEC, int G>
+__global__ __launch_bounds__(kBlock) void k_ell(int64_t R, int64_t K, const int32_t *__restrict__ ec,
+                                                const float *__restrict__ ev,
+                                                const float *__restrict__ X, int64_t ldx,
+                                                float *__restrict__ Y, int64_t ldy, int64_t F,
+                                                int64_t n_tiles)
+{
+    constexpr int GPB = kBlock / G;
+    const int g = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t c0 = (int64_t)blockIdx.y * (G * VEC) + (int64_t)lane * VEC;
+    const bool active = c0 < F;
+    const int64_t row = xcd_tile(blockIdx.x, n_tiles) * GPB + g;
+    if (row >= R) return;
+    const int gbase = (threadIdx.x % kWave) / G * G;
+    Acc<VEC> a0, a1;
+    a0.zero();
+    a1.zero();
+    for (int64_t kb = 0; kb < K; kb += G) {
+        const int64_t k = kb + lane;
+        int cj = -1;
+        float vj = 0.0f;
+        if (k < K) {
+            cj = ld_stream(ec + k * R + row);
+            vj = ld_stream(ev + k * R + row);
+        }
+        // entries are packed to the front: the stored ones form a prefix
+        const unsigned long long live =
+            (__ballot(cj >= 0) >> gbase) & (G == 64 ? ~0ull : ((1ull << G) - 1));
+        const int n = __popcll(live);
+        int j = 0;
+        for (; j + 2 <= n; j += 2) {
+            const int c_0 = __shfl(cj, j, G), c_1 = __shfl(cj, j + 1, G);
+            const float v_0 = __shfl(vj, j, G), v_1 = __shfl(vj, j + 1, G);
+            if (active) {
+                const Vec<VEC> x0 = ld_vec<VEC>(X + (int64_t)c_0 * ldx + c0);
+                const Vec<VEC> x1 = ld_vec<VEC>(X + (int64_t)c_1 * ldx + c0);
+                a0.fma(v_0, x0);
+                a1.fma(v_1, x1);
+            }
+        }
+        if (j < n) {
+            const int c_0 = __shfl(cj, j, G);
+            const float v_0 = __shfl(vj, j, G);
+            if (active) a0.fma(v_0, ld_vec<VEC>(X + (int64_t)c_0 * ldx + c0));
+        }
+        if (n < G) break;
+    }
+    a0.add(a1);
+    if (active) st_vec_stream<VEC>(Y + row * ldy + c0, a0.vec());
+}
+
+// ---------------------------------------------------------------- DIA
+// One group per row; diagonal d contributes data[d*R+i] * X[i + off_d].
+// Padding slots hold +0 and are skipped, as are columns outside [0, C).
+
+template <int VEC, int G>
+__global__ __launch_bounds__(kBlock) void k_dia(int64_t R, int64_t C, int64_t ND,
+                                                const int32_t *__restrict__ offsets,
+                                                const float *__restrict__ data,
+                                                const float *__restrict__ X, int64_t ldx,
+                                                float *__restrict__ Y, int64_t ldy, int64_t F,
+                                                int64_t n_tiles)
+{
+    constexpr int GPB = kBlock / G;
+    const int g = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t c0 = (int64_t)blockIdx.y * (G * VEC) + (int64_t)lane * VEC;
+    const bool active = c0 < F;
+    const int64_t row = xcd_tile(blockIdx.x, n_tiles) * GPB + g;
+    if (row >= R) return;
+    Acc<VEC> a0, a1;
+    a0.zero();
+    a1.zero();
+    int64_t d = 0;
+    for (; d + 2 <= ND; d += 2) {
+        const int64_t j0 = row + offsets[d], j1 = row + offsets[d + 1];
+        const float v0 = ld_stream(data + d * R + row);
+        const float v1 = ld_stream(data + (d + 1) * R + row);
+        if (active) {
+            if (v0 != 0.0f && j0 >= 0 && j0 < C) a0.fma(v0, ld_vec<VEC>(X + j0 * ldx + c0));
+            if (v1 != 0.0f && j1 >= 0 && j1 < C) a1.fma(v1, ld_vec<VEC>(X + j1 * ldx + c0));
+        }
+    }
+    if (d < ND) {
+        const int64_t j0 = row + offsets[d];
+        const float v0 = ld_stream(data + d * R + row);
+        if (active && v0 != 0.0f && j0 >= 0 && j0 < C) a0.fma(v0, ld_vec<VEC>(X + j0 * ldx + c0));
+    }
+    a0.add(a1);
+    if (active) st_vec_stream<VEC>(Y + row * ldy + c0, a0.vec());
+}
+
+// ---------------------------------------------------------------- BSR
+// One workgroup per block row.  Lanes split F as everywhere else; the
+// kBlock/G row groups split the b rows of the block row (each thread owns
+// up to RPT rows).  Each b x b block is staged in LDS; only the block
+// columns with a nonzero (bit set in the block's column mask) gather their
+// X row, so a sparse block costs its b*b values plus its touched X rows.
+
+template <int VEC, int G, int RPT>
+__global__ __launch_bounds__(kBlock) void k_bsr(int64_t R, int64_t C, int b, int64_t nbr,
+                                                const int32_t *__restrict__ bptr,
+                                                const int32_t *__restrict__ bcol,
+                                                const float *__restrict__ bval,
+                                                const uint64_t *__restrict__ bmask,
+                                                const float *__restrict__ X, int64_t ldx,
+                                                float *__restrict__ Y, int64_t ldy, int64_t F)
+{
+    constexpr int RG = kBlock / G;  // row groups
+    __shared__ float blk_lds[64 * 64];
+    const int g = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t c0 = (int64_t)blockIdx.y * (G * VEC) + (int64_t)lane * VEC;
+    const bool active = c0 < F;
+    const int64_t br = xcd_tile(blockIdx.x, nbr);
+    const int bb = b * b;
+    Acc<VEC> acc[RPT];
+#pragma unroll
+    for (int r = 0; r < RPT; r++) acc[r].zero();
+    for (int64_t blk = bptr[br]; blk < bptr[br + 1]; blk++) {
+        __syncthreads();
+        for (int t = threadIdx.x; t < bb; t += kBlock) blk_lds[t] = ld_stream(bval + blk * bb + t);
+        __syncthreads();
+        uint64_t mask = bmask[blk];
+        const int64_t xc = (int64_t)bcol[blk] * b;
+        while (mask) {
+            const int j = __ffsll((unsigned long long)mask) - 1;
+            mask &= mask - 1;
+            if (!active) continue;
+            const Vec<VEC> x = ld_vec<VEC>(X + (xc + j) * ldx + c0);
+#pragma unroll
+            for (int r = 0; r < RPT; r++) {
+                const int rr = g + r * RG;
+                if (rr < b) acc[r].fma(blk_lds[rr * b + j], x);
+            }
+        }
+    }
+    if (!active) return;
+#pragma unroll
+    for (int r = 0; r < RPT; r++) {
+        const int rr = g + r * RG;
+        const int64_t row = br * b + rr;
+        if (rr < b && row < R) st_vec_stream<VEC>(Y + row * ldy + c0, acc[r].vec());
+    }
+}
+
+// ----------------------------------------------------------- dispatch
+
+struct Shape {
+    int vec;
+    int g;
+    int64_t fslices;  // grid.y
+};
+
+Shape pick_shape(const float *X, int64_t ldx, const float *Y, int64_t ldy, int64_t F)
+{
+    auto al = [](const void *p, int n) { return ((uintptr_t)p % n) == 0; };
+    int vec = 1;
+    if (F % 4 == 0 && ldx % 4 == 0 && ldy % 4 == 0 && al(X, 16) && al(Y, 16))
+        vec = 4;
+    else if (F % 2 == 0 && ldx % 2 == 0 && ldy % 2 == 0 && al(X, 8) && al(Y, 8))
+        vec = 2;
+    const int64_t lanes = ceil_div(F, vec);
+    const int g = lanes <= 8 ? 8 : lanes <= 16 ? 16 : lanes <= 32 ? 32 : 64;
+    return Shape{vec, g, ceil_div(F, (int64_t)g * vec)};
+}
+
+// Calls fn.template operator()<VEC, G>() for the runtime (vec, g).
+template <class Fn>
+void dispatch(const Shape &sh, Fn &&fn)
+{
+#define GS_CASE(V, GG) \
+    if (sh.vec == V && sh.g == GG) return fn.template operator()<V, GG>();
+    GS_CASE(4, 8) GS_CASE(4, 16) GS_CASE(4, 32) GS_CASE(4, 64)
+    GS_CASE(2, 8) GS_CASE(2, 16) GS_CASE(2, 32) GS_CASE(2, 64)
+    GS_CASE(1, 8) GS_CASE(1, 16) GS_CASE(1, 32) GS_CASE(1, 64)
+#undef GS_CASE
+    fail(GS_ERR_UNSUPPORTED, "no kernel for vec=%d g=%d", sh.vec, sh.g);
+}
+
+unsigned u32_grid(int64_t n)
+{
+    if (n > 0x7fffffffll) fail(GS_ERR_UNSUPPORTED, "grid of %lld workgroups is too large", (long long)n);
+    return (unsigned)(n < 1 ? 1 : n);
+}
+
+int env_int(const char *name, int dflt)
+{
+    const char *v = std::getenv(name);
+    if (!v || !*v) return dflt;
+    int x = std::atoi(v);
+    return x > 0 ? x : dflt;
+}
+
+}  // namespace
+
+// --------------------------------------------------------------- plans
+
+void plan_csr(gs_matrix_ &m, hipStream_t s)
+{
+    const int thr = env_int("GS_CSR_LONG_ROW", kCsrLongRow);
+    const int chunk = env_int("GS_CSR_CHUNK", kCsrChunk);
+    m.csr_long_thr = thr;
+    m.csr_chunk = chunk;
+    std::vector<int32_t> rp((size_t)m.R + 1);
+    GS_HIP(hipMemcpyAsync(rp.data(), m.row_ptr.p, rp.size() * 4, hipMemcpyDeviceToHost, s));
+    GS_HIP(hipStreamSynchronize(s));
+    std::vector<int32_t> rows, first, chunk_of;
+    for (int64_t i = 0; i < m.R; i++) {
+        const int64_t len = rp[i + 1] - rp[i];
+        if (len > thr) {
+            first.push_back((int32_t)chunk_of.size());
+            const int64_t nc = ceil_div(len, chunk);
+            for (int64_t c = 0; c < nc; c++) chunk_of.push_back((int32_t)rows.size());
+            rows.push_back((int32_t)i);
+        }
+    }
+    first.push_back((int32_t)chunk_of.size());
+    m.n_long_rows = (int64_t)rows.size();
+    m.n_long_chunks = (int64_t)chunk_of.size();
+    m.long_rows.alloc(rows.size() * 4, s);
+    m.long_first.alloc(first.size() * 4, s);
+    m.long_chunk.alloc(chunk_of.size() * 4, s);
+    if (!rows.empty()) {
+        GS_HIP(hipMemcpyAsync(m.long_rows.p, rows.data(), rows.size() * 4, hipMemcpyHostToDevice, s));
+        GS_HIP(hipMemcpyAsync(m.long_chunk.p, chunk_of.data(), chunk_of.size() * 4,
+                              hipMemcpyHostToDevice, s));
+    }
+    GS_HIP(hipMemcpyAsync(m.long_first.p, first.data(), first.size() * 4, hipMemcpyHostToDevice, s));
+    GS_HIP(hipStreamSynchronize(s));
+}
+
+void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s)
+{
+    m.coo_chunk = env_int("GS_COO_CHUNK", kCooChunk);
+    std::vector<int32_t> rp((size_t)m.R + 1);
+    GS_HIP(hipMemcpyAsync(rp.data(), row_ptr, rp.size() * 4, hipMemcpyDeviceToHost, s));
+    GS_HIP(hipStreamSynchronize(s));
+    std::vector<int32_t> empty;
+    for (int64_t i = 0; i < m.R; i++)
+        if (rp[i + 1] == rp[i]) empty.push_back((int32_t)i);
+    m.n_empty_rows = (int64_t)empty.size();
+    m.empty_rows.alloc(empty.size() * 4, s);
+    if (!empty.empty()) {
+        GS_HIP(hipMemcpyAsync(m.empty_rows.p, empty.data(), empty.size() * 4, hipMemcpyHostToDevice, s));
+        GS_HIP(hipStreamSynchronize(s));
+    }
+}
+
+// --------------------------------------------------------------- launchers
+
+void spmm_csr(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+              hipStream_t s)
+{
+    const Shape sh = pick_shape(X, ldx, Y, ldy, F);
+    if (m.n_long_chunks) ensure_work(m, (size_t)m.n_long_chunks * F * 4, s);
+    dispatch(sh, [&]<int VEC, int G>() {
+        constexpr int GPB = kBlock / G;
+        const int64_t row_tiles = ceil_div(m.R, GPB);
+        const int64_t chunk_tiles = ceil_div(m.n_long_chunks, GPB);
+        dim3 grid(u32_grid(row_tiles + chunk_tiles), (unsigned)sh.fslices);
+        k_csr_main<VEC, G><<<grid, kBlock, 0, s>>>(
+            m.R, m.row_ptr.as<int32_t>(), m.col.as<int32_t>(), m.val.as<float>(), X, ldx, Y, ldy, F,
+            m.csr_long_thr, row_tiles, m.long_rows.as<int32_t>(), m.long_chunk.as<int32_t>(),
+            m.long_first.as<int32_t>(), m.n_long_chunks, m.csr_chunk, m.work.as<float>());
+        GS_HIP(hipGetLastError());
+        if (m.n_long_rows) {
+            dim3 g2(u32_grid(ceil_div(m.n_long_rows, GPB)), (unsigned)sh.fslices);
+            k_csr_combine<VEC, G><<<g2, kBlock, 0, s>>>(m.long_rows.as<int32_t>(),
+                                                        m.long_first.as<int32_t>(), m.n_long_rows,
+                                                        m.work.as<float>(), Y, ldy, F);
+            GS_HIP(hipGetLastError());
+        }
+    });
+}
+
+void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+              hipStream_t s)
+{
+    const Shape sh = pick_shape(X, ldx, Y, ldy, F);
+    const int chunk = m.coo_chunk;
+    const int64_t n_chunks = ceil_div(m.Z, chunk);
+    if (n_chunks) ensure_work(m, (size_t)n_chunks * 2 * F * 4, s);
+    dispatch(sh, [&]<int VEC, int G>() {
+        constexpr int GPB = kBlock / G;
+        if (n_chunks) {
+            dim3 grid(u32_grid(ceil_div(n_chunks, GPB)), (unsigned)sh.fslices);
+            k_coo_main<VEC, G><<<grid, kBlock, 0, s>>>(m.Z, m.row.as<int32_t>(), m.col.as<int32_t>(),
+                                                       m.val.as<float>(), X, ldx, Y, ldy, F, chunk,
+                                                       n_chunks, m.work.as<float>());
+            GS_HIP(hipGetLastError());
+        }
+        const int64_t groups = n_chunks + m.n_empty_rows;
+        if (groups) {
+            dim3 g2(u32_grid(ceil_div(groups, GPB)), (unsigned)sh.fslices);
+            k_coo_fixup<VEC, G><<<g2, kBlock, 0, s>>>(m.Z, m.row.as<int32_t>(), chunk, n_chunks,
+                                                      m.work.as<float>(), m.empty_rows.as<int32_t>(),
+                                                      m.n_empty_rows, Y, ldy, F);
+            GS_HIP(hipGetLastError());
+        }
+    });
+}
+
+void spmm_ell(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+              hipStream_t s)
+{
+    const Shape sh = pick_shape(X, ldx, Y, ldy, F);
+    dispatch(sh, [&]<int VEC, int G>() {
+        constexpr int GPB = kBlock / G;
+        const int64_t tiles = ceil_div(m.R, GPB);
+        if (!tiles) return;
+        dim3 grid(u32_grid(tiles), (unsigned)sh.fslices);
+        k_ell<VEC, G><<<grid, kBlock, 0, s>>>(m.R, m.K, m.ell_col.as<int32_t>(), m.ell_val.as<float>(),
+                                              X, ldx, Y, ldy, F, tiles);
+        GS_HIP(hipGetLastError());
+    });
+}
+
+void spmm_dia(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+              hipStream_t s)
+{
+    const Shape sh = pick_shape(X, ldx, Y, ldy, F);
+    dispatch(sh, [&]<int VEC, int G>() {
+        constexpr int GPB = kBlock / G;
+        const int64_t tiles = ceil_div(m.R, GPB);
+        if (!tiles) return;
+        dim3 grid(u32_grid(tiles), (unsigned)sh.fslices);
+        k_dia<VEC, G><<<grid, kBlock, 0, s>>>(m.R, m.C, m.ND, m.offsets.as<int32_t>(), m.dia.as<float>(),
+                                              X, ldx, Y, ldy, F, tiles);
+        GS_HIP(hipGetLastError());
+    });
+}
+
+void spmm_bsr(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+              hipStream_t s)
+{
+    const Shape sh = pick_shape(X, ldx, Y, ldy, F);
+    const int64_t nbr = ceil_div(m.R, m.b);
+    if (!nbr) return;
+    dispatch(sh, [&]<int VEC, int G>() {
+        constexpr int RG = kBlock / G;
+        const int rpt = (int)ceil_div(m.b, RG);
+        dim3 grid(u32_grid(nbr), (unsigned)sh.fslices);
+        auto go = [&](auto rpt_tag) {
+            constexpr int RPT = decltype(rpt_tag)::value;
+            k_bsr<VEC, G, RPT><<<grid, kBlock, 0, s>>>(m.R, m.C, m.b, nbr, m.bptr.as<int32_t>(),
+                                                       m.bcol.as<int32_t>(), m.bval.as<float>(),
+                                                       m.bmask.as<uint64_t>(), X, ldx, Y, ldy, F);
+        };
+        if (rpt <= 1) go(std::integral_constant<int, 1>{});
+        else if (rpt <= 2) go(std::integral_constant<int, 2>{});
+        else if (rpt <= 4) go(std::integral_constant<int, 4>{});
+        else if (rpt <= 8) go(std::integral_constant<int, 8>{});
+        else go(std::integral_constant<int, 16>{});
+        GS_HIP(hipGetLastError());
+    });
+}
+
+}  // namespace gs

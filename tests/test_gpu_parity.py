@@ -1,0 +1,275 @@
+"""GPU parity: every format conversion, feature and SpMM of the HIP library
+against the CPU oracle, on the same seeded inputs.
+
+Bar: conversions and integer features bit-exact; feature doubles bitwise
+equal; SpMM within |Y - Y_ref| <= 1e-5 (|A||X|) + 1e-6 elementwise.
+"""
+import numpy as np
+import pytest
+import torch
+
+import graphgen
+import oracle
+import paper_2111_00352_amd as gs
+
+pytestmark = pytest.mark.gpu
+
+FMTS = ["csr", "coo", "ell", "dia", "bsr"]
+DEV = "cuda"
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def _host(t):
+    return t.cpu().numpy()
+
+
+class Case:
+    def __init__(self, R, C, row, col, val, X=None):
+        self.R, self.C = R, C
+        self.row, self.col, self.val = row, col, val
+        self.X = X
+        self.d_row, self.d_col, self.d_val = _dev(row), _dev(col), _dev(val)
+        orow, ocol, oval = oracle.canon(R, C, row, col, val)
+        self.crow, self.ccol, self.cval = orow, ocol, oval
+        self.rp = oracle.csr(R, orow)
+
+    def build(self, fmt, b=16, **kw):
+        return gs.build_format(self.d_row, self.d_col, self.d_val, (self.R, self.C), fmt,
+                               bsr_block=b, **kw)
+
+
+def _case_from_graph(g, shuffle_seed=None):
+    row, col, val = g.row, g.col, g.val
+    if shuffle_seed is not None:
+        row, col, val = graphgen.shuffled(row, col, val, shuffle_seed)
+    return Case(g.R, g.C, row, col, val, g.X)
+
+
+def _random_case(R, C, nnz, seed, empty=0.1, shuffle=True):
+    row, col, val = graphgen.random_coo(R, C, nnz, seed, empty_rows=empty)
+    if shuffle:
+        row, col, val = graphgen.shuffled(row, col, val, seed + 1)
+    return Case(R, C, row, col, val)
+
+
+def _bits(a):
+    a = np.ascontiguousarray(a)
+    return a.view(np.uint32) if a.dtype == np.float32 else a
+
+
+def check_layout(case, fmt, b=16):
+    m = case.build(fmt, b)
+    R, C = case.R, case.C
+    if fmt == "csr":
+        exp = [case.rp, case.ccol, case.cval]
+    elif fmt == "coo":
+        exp = [case.crow, case.ccol, case.cval]
+    elif fmt == "ell":
+        K, ec, ev = oracle.ell(R, case.rp, case.ccol, case.cval)
+        assert m.param == K
+        exp = [ec, ev]
+    elif fmt == "dia":
+        off, data = oracle.dia(R, C, case.crow, case.ccol, case.cval)
+        assert m.param == off.size
+        exp = [off, data]
+    else:
+        bp, bc, bv = oracle.bsr(R, C, b, case.crow, case.ccol, case.cval)
+        assert m.param == bc.size
+        exp = [bp, bc, bv]
+    for which, e in enumerate(exp):
+        got = _host(m.array(which))
+        assert got.size == e.size, (fmt, which)
+        assert (_bits(got) == _bits(e.astype(got.dtype))).all(), (fmt, which)
+    r, c, v = (_host(t) for t in m.to_coo())
+    assert (r == case.crow).all() and (c == case.ccol).all()
+    assert (_bits(v) == _bits(case.cval)).all()
+    return m
+
+
+def check_spmm(case, m, X, rows=None, ldx_pad=0, ldy_pad=0):
+    F = X.shape[1]
+    Xd = torch.zeros((case.C, F + ldx_pad), dtype=torch.float32, device=DEV)
+    Xd[:, :F] = _dev(X)
+    Xv = Xd[:, :F]
+    out = torch.full((case.R, F + ldy_pad), 7.0, dtype=torch.float32, device=DEV)
+    Y = m.spmm(Xv, out=out[:, :F])
+    Y2 = m.spmm(Xv)
+    torch.cuda.synchronize()
+    Yh = _host(Y)
+    assert (_bits(Yh) == _bits(_host(Y2))).all(), "SpMM not deterministic"
+    if ldy_pad:
+        assert (_host(out[:, F:]) == 7.0).all(), "columns beyond F were written"
+    if rows is None:
+        Yref, M = oracle.spmm(case.R, case.rp, case.ccol, case.cval, X)
+        ok, worst = oracle.check_spmm(Yh, Yref, M)
+    else:
+        Yref, M = oracle.spmm_rows(rows, case.rp, case.ccol, case.cval, X)
+        ok, worst = oracle.check_spmm(Yh[rows], Yref, M)
+    assert ok, f"{m.format}: worst |err|/bound = {worst}"
+    return worst
+
+
+def check_features(case):
+    ints, f = oracle.features(case.R, case.C, case.crow, case.ccol)
+    got = gs.extract_features(case.d_row, case.d_col, case.d_val, (case.R, case.C))
+    for k, v in ints.items():
+        assert got[k] == v, k
+    assert got["f"] == f.tolist()
+
+
+# ------------------------------------------------------------ scaled workloads
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_scaled_workload_all_formats(k):
+    g = graphgen.scaled(k)
+    case = _case_from_graph(g)
+    check_features(case)
+    for fmt in FMTS:
+        m = check_layout(case, fmt)
+        check_spmm(case, m, g.X)
+
+
+def test_unsorted_input_is_canonicalised():
+    case = _case_from_graph(graphgen.scaled(2), shuffle_seed=9)
+    for fmt in FMTS:
+        check_layout(case, fmt)
+    check_features(case)
+
+
+# -------------------------------------------------------- property cases
+
+PROPS = [
+    (1, 1, 1, 0), (5, 7, 9, 1), (33, 17, 100, 2), (100, 100, 0, 3), (257, 129, 3000, 4),
+    (16, 16, 256, 5), (31, 64, 400, 6), (1000, 999, 8000, 7), (3000, 40, 20000, 8),
+    (40, 3000, 20000, 9),
+]
+
+
+@pytest.mark.parametrize("R,C,nnz,seed", PROPS)
+def test_random_matrix_layouts_features(R, C, nnz, seed):
+    case = _random_case(R, C, nnz, seed)
+    for fmt in FMTS:
+        for b in ((1, 3, 16, 64) if fmt == "bsr" else (16,)):
+            check_layout(case, fmt, b)
+    check_features(case)
+
+
+@pytest.mark.parametrize("F", [1, 3, 6, 64, 100, 128, 300])
+@pytest.mark.parametrize("fmt", FMTS)
+def test_spmm_widths(fmt, F):
+    case = _random_case(523, 411, 6000, 11, empty=0.2)
+    X = graphgen.features_x(case.C, F, 12, "normal")
+    m = case.build(fmt)
+    check_spmm(case, m, X)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_spmm_strided_operands(fmt):
+    case = _random_case(300, 280, 3000, 13)
+    X = graphgen.features_x(case.C, 64, 14, "normal")
+    m = case.build(fmt)
+    check_spmm(case, m, X, ldx_pad=4, ldy_pad=8)
+    check_spmm(case, m, graphgen.features_x(case.C, 20, 15), ldx_pad=1, ldy_pad=3)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_long_and_dense_rows(fmt):
+    # rows far longer than one chunk and one dense column block
+    R, C = 700, 5000
+    row, col, val = graphgen.dense_rows_coo(R, C, [0, 3, 350, 699], seed=21, base_nnz=8000)
+    case = Case(R, C, row, col, val)
+    X = graphgen.features_x(C, 32, 22, "normal")
+    try:
+        m = case.build(fmt)
+    except gs.GnnSpmmError as e:  # padded formats may be over the default cap: not here
+        raise AssertionError(str(e))
+    check_spmm(case, m, X)
+
+
+def test_empty_and_degenerate_matrices():
+    for R, C in ((0, 0), (0, 5), (5, 0), (7, 9)):
+        case = Case(R, C, np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
+        for fmt in FMTS:
+            m = case.build(fmt)
+            assert m.nnz == 0
+            if R and C:
+                Y = m.spmm(_dev(np.ones((C, 4), np.float32)))
+                assert (_host(Y) == 0).all()
+        if R and C:
+            check_features(case)
+
+
+def test_identity_spmm_is_exact():
+    n = 4097
+    idx = np.arange(n, dtype=np.int32)
+    case = Case(n, n, idx, idx, np.ones(n, np.float32))
+    X = graphgen.features_x(n, 64, 3, "normal")
+    for fmt in FMTS:
+        Y = _host(case.build(fmt).spmm(_dev(X)))
+        assert (_bits(Y) == _bits(X)).all(), fmt
+
+
+# ------------------------------------------------------------ error paths
+
+def test_invalid_coo_errors():
+    R = C = 8
+    def build(r, c, v):
+        return gs.build_format(_dev(np.array(r, np.int32)), _dev(np.array(c, np.int32)),
+                               _dev(np.array(v, np.float32)), (R, C), "csr")
+    for (r, c, v), code in [
+        (([0, 8], [0, 0], [1, 1]), gs.ERR_INDEX),
+        (([0, 1], [0, -1], [1, 1]), gs.ERR_INDEX),
+        (([0, 1], [0, 1], [1, -0.0]), gs.ERR_EXPLICIT_ZERO),
+        (([1, 0, 1], [2, 0, 2], [1, 1, 2]), gs.ERR_DUPLICATE),
+        (([1, 1, 9], [2, 2, 0], [0, 1, 1]), gs.ERR_INDEX),
+        (([1, 1], [2, 2], [0, 1]), gs.ERR_EXPLICIT_ZERO),
+    ]:
+        with pytest.raises(gs.GnnSpmmError) as e:
+            build(r, c, v)
+        assert e.value.code == code
+        with pytest.raises(oracle.OracleError) as eo:  # the oracle agrees
+            oracle.canon(R, C, r, c, v)
+        assert eo.value.code == code
+
+
+def test_infeasible_padded_format_reports_bytes():
+    R, C = 2000, 2000
+    row, col, val = graphgen.dense_rows_coo(R, C, [5], seed=4, base_nnz=4000)
+    case = Case(R, C, row, col, val)
+    with pytest.raises(gs.GnnSpmmError) as e:
+        case.build("ell", max_bytes=1 << 20)
+    assert e.value.code == gs.ERR_INFEASIBLE
+    assert e.value.bytes_required == 8 * R * C  # K = C (row 5 is dense)
+
+
+def test_spmm_argument_errors():
+    case = _random_case(50, 40, 200, 5)
+    m = case.build("csr")
+    X = torch.zeros((40, 8), device=DEV)
+    with pytest.raises(ValueError):
+        m.spmm(torch.zeros((39, 8), device=DEV))
+    Y = torch.zeros((50, 8), device=DEV)
+    rc = gs.lib().gs_spmm(m.handle, X.data_ptr(), 8, Y.data_ptr(), 4, 8, None)
+    assert rc == gs.ERR_INVALID_ARG  # ldy < F
+    big = torch.zeros((100, 8), device=DEV)
+    rc = gs.lib().gs_spmm(m.handle, big.data_ptr(), 8, big[10:].data_ptr(), 8, 8, None)
+    assert rc == gs.ERR_INVALID_ARG  # X and Y overlap
+
+
+# -------------------------------------------------------------- conversion
+
+@pytest.mark.parametrize("src", FMTS)
+def test_convert_between_formats(src):
+    case = _random_case(300, 310, 2500, 31)
+    m = case.build(src)
+    for dst in FMTS:
+        m2 = m.convert(dst)
+        r, c, v = (_host(t) for t in m2.to_coo())
+        assert (r == case.crow).all() and (c == case.ccol).all()
+        assert (_bits(v) == _bits(case.cval)).all()
+    f = m.features()
+    ints, fo = oracle.features(case.R, case.C, case.crow, case.ccol)
+    assert f["f"] == fo.tolist()

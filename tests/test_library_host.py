@@ -1,0 +1,122 @@
+"""Host-only checks of the C-ABI library: it loads, exports every symbol the
+header declares, and its argument checking and model parsing work without
+touching a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2111_00352_amd as gs
+from conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "gnnspmm.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gs_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(gs.library_path()):
+        from paper_2111_00352_amd import build
+        build.build()
+    return gs.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = _declared()
+    assert len(names) >= 18
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_abi_version_matches_header(L):
+    m = re.search(r"#define GS_ABI_VERSION (\d+)", open(HEADER).read())
+    assert L.gs_abi_version() == int(m.group(1))
+
+
+def test_null_arguments_rejected_without_gpu(L):
+    out = ctypes.c_void_p(123)
+    assert L.gs_build_format(None, 1, None, None, ctypes.byref(out), None) == gs.ERR_INVALID_ARG
+    assert out.value is None
+    assert b"gs_coo" in L.gs_last_error()
+    assert L.gs_spmm(None, None, 1, None, 1, 1, None) == gs.ERR_INVALID_ARG
+    assert L.gs_to_coo(None, None, None, None, None) == gs.ERR_INVALID_ARG
+    assert L.gs_get_info(None, None) == gs.ERR_INVALID_ARG
+    coo = gs._Coo(4, 4, 1, None, None, None)  # nnz > 0 with null arrays
+    assert L.gs_build_format(ctypes.byref(coo), 1, None, None, ctypes.byref(out), None) == gs.ERR_INVALID_ARG
+    coo = gs._Coo(-1, 4, 0, None, None, None)
+    assert L.gs_build_format(ctypes.byref(coo), 1, None, None, ctypes.byref(out), None) == gs.ERR_INVALID_ARG
+    coo = gs._Coo(1 << 31, 4, 0, None, None, None)
+    assert L.gs_build_format(ctypes.byref(coo), 1, None, None, ctypes.byref(out), None) == gs.ERR_UNSUPPORTED
+    coo = gs._Coo(4, 4, 0, None, None, None)
+    assert L.gs_build_format(ctypes.byref(coo), 7, None, None, ctypes.byref(out), None) == gs.ERR_INVALID_ARG
+    bad = gs._BuildOpts(65, 0, 0)
+    assert L.gs_build_format(ctypes.byref(coo), 4, ctypes.byref(bad), None, ctypes.byref(out), None) == gs.ERR_INVALID_ARG
+
+
+def _ctx(L, **kw):
+    o = gs._SelOpts(kw.get("mode", 0), kw.get("fixed", 1), kw.get("path"), 0, kw.get("b", 16), 3)
+    h = ctypes.c_void_p()
+    rc = L.gs_ctx_create(ctypes.byref(o), ctypes.byref(h))
+    return rc, h
+
+
+def test_context_creation_and_builtin_model(L):
+    rc, h = _ctx(L)
+    assert rc == 0 and h.value
+    st = gs._SelStats()
+    assert L.gs_ctx_stats(h, ctypes.byref(st)) == 0
+    L.gs_ctx_destroy(h)
+    assert _ctx(L, mode=5)[0] == gs.ERR_INVALID_ARG
+    assert _ctx(L, fixed=9)[0] == gs.ERR_INVALID_ARG
+    assert _ctx(L, b=0)[0] == 0
+    assert _ctx(L, b=99)[0] == gs.ERR_INVALID_ARG
+
+
+MODEL_OK = """GSMODEL 1
+nfeat 21
+classes 2 1 3
+min """ + " ".join(["0"] * 21) + """
+max """ + " ".join(["1"] * 21) + """
+base 0.5 0
+ntrees 1
+tree 1 3
+12 0.9 1 2 0
+-1 0 0 0 0
+-1 0 0 0 1
+"""
+
+
+@pytest.mark.parametrize("text,code", [
+    (MODEL_OK, 0),
+    ("", gs.ERR_MODEL),
+    ("GSMODEL 2\n", gs.ERR_MODEL),
+    (MODEL_OK.replace("nfeat 21", "nfeat 20"), gs.ERR_MODEL),
+    (MODEL_OK.replace("classes 2 1 3", "classes 2 1 9"), gs.ERR_MODEL),
+    (MODEL_OK.replace("12 0.9 1 2 0", "12 0.9 0 2 0"), gs.ERR_MODEL),   # child not after parent
+    (MODEL_OK.replace("12 0.9 1 2 0", "30 0.9 1 2 0"), gs.ERR_MODEL),   # feature index
+    (MODEL_OK.replace("tree 1 3", "tree 1 4"), gs.ERR_MODEL),           # short node list
+])
+def test_model_file_parsing(L, tmp_path, text, code):
+    p = tmp_path / "m.gsm"
+    p.write_text(text)
+    rc, h = _ctx(L, path=str(p).encode())
+    assert rc == code, L.gs_last_error()
+    if rc == 0:
+        L.gs_ctx_destroy(h)
+
+
+def test_missing_model_file(L, tmp_path):
+    rc, _ = _ctx(L, path=str(tmp_path / "absent.gsm").encode())
+    assert rc == gs.ERR_MODEL
+
+
+def test_allocator_hooks_must_be_paired(L):
+    a = gs._Allocator(gs._ALLOC_FN(lambda n, s, c: None), gs._FREE_FN(), None)
+    assert L.gs_set_allocator(ctypes.byref(a)) == gs.ERR_INVALID_ARG
+    assert L.gs_set_allocator(None) == 0
