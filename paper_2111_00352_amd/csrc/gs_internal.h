@@ -112,8 +112,10 @@ struct gs_matrix_ {
     int csr_long_thr = 0, csr_chunk = 0, coo_chunk = 0;
     int64_t n_long_rows = 0, n_long_chunks = 0;
     gs::DevBuf long_rows;    // int32 row ids, n_long_rows
-    gs::DevBuf long_chunk;   // int32 [n_long_chunks] -> index into long_rows
-    gs::DevBuf long_first;   // int32 [n_long_rows+1] -> first chunk of each long row
+    gs::DevBuf long_first;   // int32 [n_long_rows+1] -> first partial slot of each long row
+    gs::DevBuf csr_items;    // int4 {row, start, len, slot} work items
+    int64_t n_items = 0;
+    bool csr_sorted = false; // items ordered by decreasing length
     // COO: rows with no entries (zeroed by the COO kernel)
     int64_t n_empty_rows = 0;
     gs::DevBuf empty_rows;
@@ -130,10 +132,10 @@ constexpr uint64_t kDefaultMaxBytes = 8ull << 30;
 constexpr int kDefaultBsrBlock = 16;
 
 // Rows longer than this go through the split (multi-workgroup) CSR path.
-constexpr int kCsrLongRow = 256;
+constexpr int kCsrLongRow = 64;
 // Chunk length of the split CSR path and of the COO segmented reduction.
-constexpr int kCsrChunk = 256;
-constexpr int kCooChunk = 256;
+constexpr int kCsrChunk = 64;
+constexpr int kCooChunk = 128;
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -194,6 +196,20 @@ void spmm_bsr(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
 // Plans built at conversion time for the CSR and COO kernels.
 void plan_csr(gs_matrix_ &m, hipStream_t s);
 void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s);
+
+// Vectorised CSR path; returns false when F / alignment do not allow it.
+bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+                   hipStream_t s);
+
+// Workgroups of 256 threads the device keeps resident at full occupancy
+// (compute units x 8), queried once.
+int resident_workgroups();
+
+// Vectorised ELL / DIA paths; false when F / alignment do not allow them.
+bool spmm_ell_fast(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+                   hipStream_t s);
+bool spmm_dia_fast(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+                   hipStream_t s);
 
 // Makes sure m.work holds at least bytes (reallocating in stream order).
 void ensure_work(gs_matrix_ &m, size_t bytes, hipStream_t s);

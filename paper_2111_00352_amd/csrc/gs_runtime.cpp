@@ -68,6 +68,18 @@ void ensure_work(gs_matrix_ &m, size_t bytes, hipStream_t s)
     m.work.alloc(bytes, s);
 }
 
+int resident_workgroups()
+{
+    static int n = 0;
+    if (n == 0) {
+        int dev = 0, cus = 0;
+        GS_HIP(hipGetDevice(&dev));
+        GS_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+        n = (cus > 0 ? cus : 256) * 8;
+    }
+    return n;
+}
+
 }  // namespace gs
 
 using namespace gs;

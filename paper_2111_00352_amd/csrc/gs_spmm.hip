@@ -106,42 +106,29 @@ __device__ __forceinline__ Acc<VEC> gather_range(const int32_t *__restrict__ col
 }
 
 // ---------------------------------------------------------------- CSR
-// Blocks [0, n_row_tiles): one group per row for rows of at most long_thr
-// entries.  Blocks [n_row_tiles, ...): one group per chunk of a long row,
-// writing its partial sum to work[chunk * F + c].
+// Generic path (any F and alignment): one group per work item {row, start,
+// len, slot} of the CSR plan; slot >= 0 items are chunks of long rows whose
+// partial sums go to work[slot * F + c].
 
 template <int VEC, int G>
-__global__ __launch_bounds__(kBlock) void k_csr_main(
-    int64_t R, const int32_t *__restrict__ rp, const int32_t *__restrict__ col,
-    const float *__restrict__ val, const float *__restrict__ X, int64_t ldx,
-    float *__restrict__ Y, int64_t ldy, int64_t F, int long_thr, int64_t n_row_tiles,
-    const int32_t *__restrict__ long_rows, const int32_t *__restrict__ long_chunk,
-    const int32_t *__restrict__ long_first, int64_t n_chunks, int chunk_len,
-    float *__restrict__ work)
+__global__ __launch_bounds__(kBlock) void k_csr_items_generic(
+    int64_t n_items, const int4 *__restrict__ items, const int32_t *__restrict__ col,
+    const float *__restrict__ val, const float *__restrict__ X, int64_t ldx, float *__restrict__ Y,
+    int64_t ldy, int64_t F, float *__restrict__ work)
 {
-    constexpr int GPB = kBlock / G;  // groups per block
+    constexpr int GPB = kBlock / G;
     const int g = threadIdx.x / G, lane = threadIdx.x % G;
     const int64_t c0 = (int64_t)blockIdx.y * (G * VEC) + (int64_t)lane * VEC;
     const bool active = c0 < F;
-    const int64_t bid = blockIdx.x;
-    if (bid < n_row_tiles) {
-        const int64_t row = xcd_tile(bid, n_row_tiles) * GPB + g;
-        if (row >= R) return;
-        const int64_t s = rp[row], e = rp[row + 1];
-        if (e - s > long_thr) return;
-        Acc<VEC> acc = gather_range<VEC, G>(col, val, s, e, X, ldx, c0, active, lane);
-        if (active) st_vec_stream<VEC>(Y + row * ldy + c0, acc.vec());
-    } else {
-        const int64_t ch = (bid - n_row_tiles) * GPB + g;
-        if (ch >= n_chunks) return;
-        const int lr = long_chunk[ch];
-        const int64_t row = long_rows[lr];
-        const int64_t s = rp[row] + (ch - long_first[lr]) * (int64_t)chunk_len;
-        int64_t e = s + chunk_len;
-        if (e > rp[row + 1]) e = rp[row + 1];
-        Acc<VEC> acc = gather_range<VEC, G>(col, val, s, e, X, ldx, c0, active, lane);
-        if (active) st_vec<VEC>(work + ch * F + c0, acc.vec());
-    }
+    const int64_t it = (int64_t)blockIdx.x * GPB + g;
+    if (it >= n_items) return;
+    const int4 d = items[it];
+    Acc<VEC> acc = gather_range<VEC, G>(col, val, d.y, (int64_t)d.y + d.z, X, ldx, c0, active, lane);
+    if (!active) return;
+    if (d.w < 0)
+        st_vec_stream<VEC>(Y + (int64_t)d.x * ldy + c0, acc.vec());
+    else
+        st_vec<VEC>(work + (int64_t)d.w * F + c0, acc.vec());
 }
 
 // One group per long row: sums its chunks' partials in chunk order.
@@ -232,19 +219,35 @@ __global__ __launch_bounds__(kBlock) void k_coo_main(int64_t Z, const int32_t *_
         const unsigned long long heads =
             (__ballot(starts) >> gbase) & (G == 64 ? ~0ull : ((1ull << G) - 1));
         const int n = (int)((k1 - kb) < G ? (k1 - kb) : G);
-        for (int j = 0; j < n; j++) {
-            const int r_j = __shfl(rj, j, G);
-            const int c_j = __shfl(cj, j, G);
-            const float v_j = __shfl(vj, j, G);
-            if ((j == 0 && r_j != cur) || ((heads >> j) & 1ull)) {
-                // the row changes before entry j: flush the finished segment
-                coo_flush<VEC>(acc, cur, first_seg, false, head_cont, tail_cont, q, Y, ldy, work,
-                               F, c0, active);
-                first_seg = false;
-                acc.zero();
-                cur = r_j;
+        // X rows of UB entries are requested before any of them is consumed;
+        // entries past n gather row 0 of X (a valid row) and are skipped.
+        constexpr int UB = 8;
+        for (int j0 = 0; j0 < n; j0 += UB) {
+            Vec<VEC> xs[UB];
+            float vs[UB];
+            int rs[UB];
+#pragma unroll
+            for (int u = 0; u < UB; u++) {
+                const int j = j0 + u;
+                const int c_u = __shfl(cj, j, G);
+                vs[u] = __shfl(vj, j, G);
+                rs[u] = __shfl(rj, j, G);
+                if (active) xs[u] = ld_vec<VEC>(X + (int64_t)c_u * ldx + c0);
             }
-            if (active) acc.fma(v_j, ld_vec<VEC>(X + (int64_t)c_j * ldx + c0));
+#pragma unroll
+            for (int u = 0; u < UB; u++) {
+                const int j = j0 + u;
+                if (j >= n) break;
+                if ((j == 0 && rs[u] != cur) || ((heads >> j) & 1ull)) {
+                    // the row changes before entry j: flush the finished segment
+                    coo_flush<VEC>(acc, cur, first_seg, false, head_cont, tail_cont, q, Y, ldy,
+                                   work, F, c0, active);
+                    first_seg = false;
+                    acc.zero();
+                    cur = rs[u];
+                }
+                if (active) acc.fma(vs[u], xs[u]);
+            }
         }
     }
     coo_flush<VEC>(acc, cur, first_seg, true, head_cont, tail_cont, q, Y, ldy, work, F, c0,
@@ -489,7 +492,7 @@ unsigned u32_grid(int64_t n)
     return (unsigned)(n < 1 ? 1 : n);
 }
 
-int env_int(const char *name, int dflt)
+int env_int_coo(const char *name, int dflt)
 {
     const char *v = std::getenv(name);
     if (!v || !*v) return dflt;
@@ -501,43 +504,9 @@ int env_int(const char *name, int dflt)
 
 // --------------------------------------------------------------- plans
 
-void plan_csr(gs_matrix_ &m, hipStream_t s)
-{
-    const int thr = env_int("GS_CSR_LONG_ROW", kCsrLongRow);
-    const int chunk = env_int("GS_CSR_CHUNK", kCsrChunk);
-    m.csr_long_thr = thr;
-    m.csr_chunk = chunk;
-    std::vector<int32_t> rp((size_t)m.R + 1);
-    GS_HIP(hipMemcpyAsync(rp.data(), m.row_ptr.p, rp.size() * 4, hipMemcpyDeviceToHost, s));
-    GS_HIP(hipStreamSynchronize(s));
-    std::vector<int32_t> rows, first, chunk_of;
-    for (int64_t i = 0; i < m.R; i++) {
-        const int64_t len = rp[i + 1] - rp[i];
-        if (len > thr) {
-            first.push_back((int32_t)chunk_of.size());
-            const int64_t nc = ceil_div(len, chunk);
-            for (int64_t c = 0; c < nc; c++) chunk_of.push_back((int32_t)rows.size());
-            rows.push_back((int32_t)i);
-        }
-    }
-    first.push_back((int32_t)chunk_of.size());
-    m.n_long_rows = (int64_t)rows.size();
-    m.n_long_chunks = (int64_t)chunk_of.size();
-    m.long_rows.alloc(rows.size() * 4, s);
-    m.long_first.alloc(first.size() * 4, s);
-    m.long_chunk.alloc(chunk_of.size() * 4, s);
-    if (!rows.empty()) {
-        GS_HIP(hipMemcpyAsync(m.long_rows.p, rows.data(), rows.size() * 4, hipMemcpyHostToDevice, s));
-        GS_HIP(hipMemcpyAsync(m.long_chunk.p, chunk_of.data(), chunk_of.size() * 4,
-                              hipMemcpyHostToDevice, s));
-    }
-    GS_HIP(hipMemcpyAsync(m.long_first.p, first.data(), first.size() * 4, hipMemcpyHostToDevice, s));
-    GS_HIP(hipStreamSynchronize(s));
-}
-
 void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s)
 {
-    m.coo_chunk = env_int("GS_COO_CHUNK", kCooChunk);
+    m.coo_chunk = env_int_coo("GS_COO_CHUNK", kCooChunk);
     std::vector<int32_t> rp((size_t)m.R + 1);
     GS_HIP(hipMemcpyAsync(rp.data(), row_ptr, rp.size() * 4, hipMemcpyDeviceToHost, s));
     GS_HIP(hipStreamSynchronize(s));
@@ -557,18 +526,18 @@ void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s)
 void spmm_csr(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
               hipStream_t s)
 {
+    if (spmm_csr_vec4(m, X, ldx, Y, ldy, F, s)) return;
     const Shape sh = pick_shape(X, ldx, Y, ldy, F);
     if (m.n_long_chunks) ensure_work(m, (size_t)m.n_long_chunks * F * 4, s);
     dispatch(sh, [&]<int VEC, int G>() {
         constexpr int GPB = kBlock / G;
-        const int64_t row_tiles = ceil_div(m.R, GPB);
-        const int64_t chunk_tiles = ceil_div(m.n_long_chunks, GPB);
-        dim3 grid(u32_grid(row_tiles + chunk_tiles), (unsigned)sh.fslices);
-        k_csr_main<VEC, G><<<grid, kBlock, 0, s>>>(
-            m.R, m.row_ptr.as<int32_t>(), m.col.as<int32_t>(), m.val.as<float>(), X, ldx, Y, ldy, F,
-            m.csr_long_thr, row_tiles, m.long_rows.as<int32_t>(), m.long_chunk.as<int32_t>(),
-            m.long_first.as<int32_t>(), m.n_long_chunks, m.csr_chunk, m.work.as<float>());
-        GS_HIP(hipGetLastError());
+        if (m.n_items) {
+            dim3 grid(u32_grid(ceil_div(m.n_items, GPB)), (unsigned)sh.fslices);
+            k_csr_items_generic<VEC, G><<<grid, kBlock, 0, s>>>(
+                m.n_items, m.csr_items.as<int4>(), m.col.as<int32_t>(), m.val.as<float>(), X, ldx, Y,
+                ldy, F, m.work.as<float>());
+            GS_HIP(hipGetLastError());
+        }
         if (m.n_long_rows) {
             dim3 g2(u32_grid(ceil_div(m.n_long_rows, GPB)), (unsigned)sh.fslices);
             k_csr_combine<VEC, G><<<g2, kBlock, 0, s>>>(m.long_rows.as<int32_t>(),
@@ -609,6 +578,7 @@ void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
 void spmm_ell(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
               hipStream_t s)
 {
+    if (spmm_ell_fast(m, X, ldx, Y, ldy, F, s)) return;
     const Shape sh = pick_shape(X, ldx, Y, ldy, F);
     dispatch(sh, [&]<int VEC, int G>() {
         constexpr int GPB = kBlock / G;
@@ -624,6 +594,7 @@ void spmm_ell(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
 void spmm_dia(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
               hipStream_t s)
 {
+    if (spmm_dia_fast(m, X, ldx, Y, ldy, F, s)) return;
     const Shape sh = pick_shape(X, ldx, Y, ldy, F);
     dispatch(sh, [&]<int VEC, int G>() {
         constexpr int GPB = kBlock / G;

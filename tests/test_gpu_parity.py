@@ -273,3 +273,26 @@ def test_convert_between_formats(src):
     f = m.features()
     ints, fo = oracle.features(case.R, case.C, case.crow, case.ccol)
     assert f["f"] == fo.tolist()
+
+
+@pytest.mark.parametrize("xs", [1, 2, 4, 8])
+@pytest.mark.parametrize("F", [64, 128, 256])
+def test_csr_xcd_slicing(monkeypatch, xs, F):
+    # the CSR kernel can pin column slices of F to XCDs; every split must agree
+    monkeypatch.setenv("GS_CSR_XSLICE", str(xs))
+    g = graphgen.scaled(2)
+    case = _case_from_graph(g)
+    X = graphgen.features_x(case.C, F, 40 + F, "normal")
+    check_spmm(case, case.build("csr"), X)
+
+
+@pytest.mark.parametrize("cpl,lif", [(4, 8), (8, 16), (16, 8), (16, 16)])
+@pytest.mark.parametrize("F", [64, 128, 256])
+def test_csr_lane_shapes(monkeypatch, cpl, lif, F):
+    # columns per lane and loads in flight are tunable; every shape must agree
+    monkeypatch.setenv("GS_CSR_CPL", str(cpl))
+    monkeypatch.setenv("GS_CSR_LIF", str(lif))
+    g = graphgen.scaled(2)
+    case = _case_from_graph(g)
+    X = graphgen.features_x(case.C, F, 50 + F, "normal")
+    check_spmm(case, case.build("csr"), X)
