@@ -766,6 +766,13 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
                     rp, col, val, R, b, nbr, m->bptr.as<int32_t>(), m->bcol.as<int32_t>(),
                     m->bval.as<float>(), m->bmask.as<uint64_t>());
                 GS_LAUNCH_CHECK();
+                // dense-block count (kernel choice at SpMM time)
+                std::vector<uint64_t> hm((size_t)nb);
+                GS_HIP(hipMemcpyAsync(hm.data(), m->bmask.p, (size_t)nb * 8, hipMemcpyDeviceToHost, s));
+                GS_HIP(hipStreamSynchronize(s));
+                int64_t dense = 0;
+                for (uint64_t x : hm) dense += __builtin_popcountll(x) >= kBsrDenseCols;
+                m->n_dense_blocks = dense;
             }
             m->device_bytes = need;
             break;

@@ -132,10 +132,12 @@ constexpr uint64_t kDefaultMaxBytes = 8ull << 30;
 constexpr int kDefaultBsrBlock = 16;
 
 // Rows longer than this go through the split (multi-workgroup) CSR path.
-constexpr int kCsrLongRow = 64;
+constexpr int kCsrLongRow = 128;
 // Chunk length of the split CSR path and of the COO segmented reduction.
-constexpr int kCsrChunk = 64;
+constexpr int kCsrChunk = 128;
 constexpr int kCooChunk = 128;
+// A 16x16 BSR block with at least this many stored columns counts as dense.
+constexpr int kBsrDenseCols = 8;
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -210,6 +212,10 @@ bool spmm_ell_fast(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
                    hipStream_t s);
 bool spmm_dia_fast(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
                    hipStream_t s);
+
+// 16x16-block BSR on the matrix cores; false when b != 16 or F % 16 != 0.
+bool spmm_bsr16_mfma(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+                     hipStream_t s);
 
 // Makes sure m.work holds at least bytes (reallocating in stream order).
 void ensure_work(gs_matrix_ &m, size_t bytes, hipStream_t s);

@@ -610,6 +610,7 @@ void spmm_dia(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
 void spmm_bsr(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
               hipStream_t s)
 {
+    if (spmm_bsr16_mfma(m, X, ldx, Y, ldy, F, s)) return;
     const Shape sh = pick_shape(X, ldx, Y, ldy, F);
     const int64_t nbr = ceil_div(m.R, m.b);
     if (!nbr) return;

@@ -131,11 +131,27 @@ __global__ __launch_bounds__(kBlock) void k_csr_combine4(const int32_t *__restri
     const int64_t lr = (int64_t)blockIdx.x * GPB + g;
     if (lr >= n_long) return;
     const int64_t c0 = (int64_t)blockIdx.y * (G * CPL) + (int64_t)lane * CPL;
+    const int64_t s0 = long_first[lr], s1 = long_first[lr + 1];
     for (int q = 0; q < NQ; q++) {
         if (c0 + 4 * q >= F) break;
+        const float *wp = work + c0 + 4 * q;
         float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int64_t sl = long_first[lr]; sl < long_first[lr + 1]; sl++) {
-            const float4 p = *reinterpret_cast<const float4 *>(work + sl * F + c0 + 4 * q);
+        int64_t sl = s0;
+        // eight partials in flight; added strictly in slot order
+        for (; sl + 8 <= s1; sl += 8) {
+            float4 p[8];
+#pragma unroll
+            for (int u = 0; u < 8; u++) p[u] = *reinterpret_cast<const float4 *>(wp + (sl + u) * F);
+#pragma unroll
+            for (int u = 0; u < 8; u++) {
+                a.x += p[u].x;
+                a.y += p[u].y;
+                a.z += p[u].z;
+                a.w += p[u].w;
+            }
+        }
+        for (; sl < s1; sl++) {
+            const float4 p = *reinterpret_cast<const float4 *>(wp + sl * F);
             a.x += p.x;
             a.y += p.y;
             a.z += p.z;

@@ -296,3 +296,25 @@ def test_csr_lane_shapes(monkeypatch, cpl, lif, F):
     case = _case_from_graph(g)
     X = graphgen.features_x(case.C, F, 50 + F, "normal")
     check_spmm(case, case.build("csr"), X)
+
+
+@pytest.mark.parametrize("F", [16, 48, 80, 512, 1040])
+def test_bsr16_matrix_core_widths(monkeypatch, F):
+    # 16x16 blocks run on the matrix cores for F a multiple of 16 (wide F
+    # spans several workgroup column groups); R, C not multiples of 16
+    monkeypatch.setenv("GS_BSR_MFMA", "1")  # force the matrix-core kernel on sparse blocks too
+    case = _random_case(1001, 997, 12000, 61, empty=0.1)
+    X = graphgen.features_x(case.C, F, 62, "normal")
+    check_spmm(case, case.build("bsr", 16), X)
+
+
+def test_bsr16_dense_blocks_match_generic(monkeypatch):
+    # block-community structure: full 16x16 diagonal blocks plus sparse ones
+    g = graphgen.scaled(4)
+    case = _case_from_graph(g)
+    m = case.build("bsr", 16)
+    monkeypatch.setenv("GS_BSR_MFMA", "1")
+    w1 = check_spmm(case, m, g.X)
+    monkeypatch.setenv("GS_BSR_GENERIC", "1")
+    w2 = check_spmm(case, m, g.X)
+    assert w1 <= 1.0 and w2 <= 1.0
