@@ -48,8 +48,11 @@ constexpr int kNFeat = 21;
 // Built-in model: hand-set score trees standing in for a trained ensemble.
 // Features are scaled by the given ranges; thresholds are in scaled units.
 // CSR is the default (base score 1); DIA wins when nearly all stored slots
-// of few diagonals are filled, ELL when rows are near-uniform and short,
-// BSR when 16x16 blocks are mostly full.
+// of few diagonals are filled (ER_DIA >= 0.6, at most 64 diagonals), ELL when
+// rows are near-uniform (cv < 0.05) and short (max_RD < 64), BSR when 16x16
+// blocks are mostly full (fill >= 0.5).  These thresholds restate what the
+// per-format SpMM timings on MI355X show; a trained ensemble in the same
+// file format replaces them through model_path.
 const char *kBuiltinModel = R"(GSMODEL 1
 nfeat 21
 classes 5 1 0 2 3 4
@@ -64,7 +67,7 @@ tree 3 5
 -1 0 0 0 2
 -1 0 0 0 -10
 tree 2 5
-17 0.003 1 2 0
+17 0.0005 1 2 0
 5 6.4e-4 3 4 0
 -1 0 0 0 -5
 -1 0 0 0 1.5

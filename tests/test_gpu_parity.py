@@ -318,3 +318,43 @@ def test_bsr16_dense_blocks_match_generic(monkeypatch):
     monkeypatch.setenv("GS_BSR_GENERIC", "1")
     w2 = check_spmm(case, m, g.X)
     assert w1 <= 1.0 and w2 <= 1.0
+
+
+# --------------------------------------------------------------- selection
+
+@pytest.mark.parametrize("mode", ["model", "profile", "fixed"])
+def test_select_and_run_modes(mode):
+    # every selection mode must return A.X (in whatever format it picks),
+    # convert at most once per key, and report what it chose
+    g = graphgen.scaled(3)
+    case = _case_from_graph(g)
+    ctx = gs.SelectContext(mode, fixed="ell")
+    shape = (case.R, case.C)
+    Yref, M = oracle.spmm(case.R, case.rp, case.ccol, case.cval, g.X)
+    X = _dev(g.X)
+    seen = set()
+    for _ in range(3):
+        Y, fmt = ctx.run(7, case.d_row, case.d_col, case.d_val, shape, X)
+        ok, worst = oracle.check_spmm(_host(Y), Yref, M)
+        assert ok, (mode, fmt, worst)
+        seen.add(fmt)
+    assert len(seen) == 1
+    st = ctx.stats()
+    assert st["chosen"] == fmt and st["feasible_mask"] & (1 << gs.FORMATS[fmt])
+    if mode == "fixed":
+        assert fmt == "ell"
+    if mode == "profile":  # the reference selector keeps the fastest measured format
+        times = {k: v for k, v in st["scores"].items() if v > 0}
+        assert min(times.values()) * 1.0101 >= times[fmt]
+    # a different width re-decides but reuses the cached features
+    X2 = _dev(graphgen.features_x(case.C, 16, 5))
+    Yref2, M2 = oracle.spmm(case.R, case.rp, case.ccol, case.cval, _host(X2))
+    Y2, _ = ctx.run(7, case.d_row, case.d_col, case.d_val, shape, X2)
+    assert oracle.check_spmm(_host(Y2), Yref2, M2)[0]
+
+
+def test_select_model_on_mesh_prefers_diagonals():
+    g = graphgen.scaled(3)
+    case = _case_from_graph(g)
+    ctx = gs.SelectContext("model")
+    assert ctx.select(1, case.d_row, case.d_col, case.d_val, (case.R, case.C), 64) == "dia"
