@@ -127,7 +127,7 @@ def _chung_lu_pairs(rng, n, gamma, mean_deg, cap):
     idx = np.arange(1, n + 1, dtype=np.float64)
     base = idx ** (-1.0 / (gamma - 1.0))
     lo, hi = 0.0, float(cap) / base[0] * 4.0 + mean_deg * n
-    for _ in range(200):
+    for _ in range(80):
         s = 0.5 * (lo + hi)
         if np.minimum(cap, s * base).mean() < mean_deg:
             lo = s

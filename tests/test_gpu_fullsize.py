@@ -1,0 +1,107 @@
+"""Full-size parity: every workload at its real shape, through the selector
+(the launch configuration the benchmark times) and through every feasible
+format, checked against the oracle on sampled rows (the hub rows, the first
+and last rows and a seeded random sample), plus exact features.
+
+The large workload's second layer takes ReLU((A X1) W) as input, built on the
+CPU from the oracle's own first-layer output."""
+import numpy as np
+import pytest
+import torch
+
+import graphgen
+import oracle
+import paper_2111_00352_amd as gs
+
+pytestmark = pytest.mark.gpu
+
+FMTS = ["csr", "coo", "ell", "dia", "bsr"]
+
+
+class Full:
+    def __init__(self, k):
+        g = graphgen.config(k)
+        self.g = g
+        self.rp = oracle.csr(g.R, g.row)
+        dev = "cuda"
+        self.row, self.col, self.val = (torch.from_numpy(a).to(dev) for a in (g.row, g.col, g.val))
+        self.X = torch.from_numpy(g.X).to(dev)
+        lens = np.diff(self.rp)
+        rng = np.random.default_rng(100 + k)
+        pick = [0, g.R - 1, int(np.argmax(lens)), int(np.argmin(lens))]
+        pick += list(np.argsort(lens)[-8:])
+        pick += list(rng.choice(g.R, size=min(g.R, 400), replace=False))
+        self.rows = np.unique(np.array(pick, dtype=np.int64))
+
+    def check(self, Y, X=None, label=""):
+        Xh = self.g.X if X is None else X
+        Yref, M = oracle.spmm_rows(self.rows, self.rp, self.g.col, self.g.val, Xh)
+        Yh = Y[torch.from_numpy(self.rows).to(Y.device)].cpu().numpy()
+        ok, worst = oracle.check_spmm(Yh, Yref, M)
+        assert ok, f"{label}: worst |err|/bound {worst}"
+        return worst
+
+
+_cache = {}
+
+
+def full(k):
+    if k not in _cache:
+        _cache.clear()
+        _cache[k] = Full(k)
+    return _cache[k]
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_fullsize_selector_and_features(k):
+    f = full(k)
+    g = f.g
+    ctx = gs.SelectContext("model")
+    Y, fmt = ctx.run(1, f.row, f.col, f.val, (g.R, g.C), f.X)
+    Y, fmt2 = ctx.run(1, f.row, f.col, f.val, (g.R, g.C), f.X)  # steady state (cached)
+    assert fmt == fmt2
+    f.check(Y, label=f"selector/{fmt}")
+    ints, feats = oracle.features(g.R, g.C, g.row, g.col)
+    got = gs.extract_features(f.row, f.col, f.val, (g.R, g.C))
+    assert all(got[n] == v for n, v in ints.items())
+    assert got["f"] == feats.tolist()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_fullsize_every_feasible_format(k):
+    f = full(k)
+    g = f.g
+    for fmt in FMTS:
+        try:
+            m = gs.build_format(f.row, f.col, f.val, (g.R, g.C), fmt)
+        except gs.GnnSpmmError as e:
+            assert e.code == gs.ERR_INFEASIBLE, str(e)
+            continue
+        f.check(m.spmm(f.X), label=fmt)
+        if fmt in ("csr", "coo"):  # canonical arrays, byte for byte
+            exp = [f.rp if fmt == "csr" else g.row, g.col, g.val]
+            for which, e in enumerate(exp):
+                got = m.array(which).cpu().numpy()
+                assert got.size == e.size and (got.view(np.uint32) == e.view(np.uint32)).all()
+        m.close()
+        torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(600)
+def test_fullsize_large_two_layers():
+    # layer 2 re-selects on the same adjacency (cache hit) with the ReLU output
+    f = full(5)
+    g = f.g
+    Y1ref, _ = oracle.spmm(g.R, f.rp, g.col, g.val, g.X)
+    W = graphgen.layer2_weight(g.F)
+    X2 = np.maximum(Y1ref.astype(np.float32) @ W, 0.0).astype(np.float32)
+    assert 0.3 < float((X2 == 0).mean()) < 0.7  # about half zeros, as specified
+    ctx = gs.SelectContext("model")
+    Y1, fmt1 = ctx.run(5, f.row, f.col, f.val, (g.R, g.C), f.X)
+    f.check(Y1, label=f"layer1/{fmt1}")
+    X2d = torch.from_numpy(X2).cuda()
+    Y2, fmt2 = ctx.run(5, f.row, f.col, f.val, (g.R, g.C), X2d)
+    assert ctx.stats()["t_convert"] >= 0
+    f.check(Y2, X=X2, label=f"layer2/{fmt2}")
