@@ -232,8 +232,14 @@ def main():
             "mode": "model",
             "chosen": chosen,
             "best_measured": best,
-            "speedup_vs_csr": round(t_csr / (t_sel * 1e6), 3),
+            # steady-state kernel speedup of the chosen format over fixed CSR,
+            # and of the best measured format (the exhaustive-search reference)
+            "speedup_vs_csr": round(t_csr / feasible[chosen]["median_us"], 3),
             "best_vs_csr": round(t_csr / feasible[best]["median_us"], 3),
+            "fraction_of_best": round(feasible[best]["median_us"] / feasible[chosen]["median_us"], 3),
+            "speedup_vs_coo": round(feasible["coo"]["median_us"] / feasible[chosen]["median_us"], 3),
+            "selector_step_us": round(t_sel * 1e6, 2),
+            "host_overhead_us": round(t_sel * 1e6 - feasible[chosen]["median_us"], 2),
             "first_call_s": round(first_call_s, 4),
             "t_features_s": round(st["t_features"], 4),
             "t_convert_s": round(st["t_convert"], 4),

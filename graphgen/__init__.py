@@ -323,3 +323,88 @@ def features_x(n: int, F: int, seed: int, kind: str = "um11") -> np.ndarray:
     if kind == "ones":
         return np.ones((n, F), np.float32)
     return _um11(rng, (n, F))
+
+
+# ---------------------------------------------------------------- training set
+# Matrices for training the format predictor.  The paper's recipe: square
+# random 0/1 matrices, sizes 1,000..15,000 in steps of 200, "sparsity" 0.1% to
+# 70%, read as density, here log-uniform and capped so that nnz <= 30M.  All
+# stored values are 1 (the paper's 0/1 matrices).
+
+TRAIN_SIZES = list(range(1000, 15001, 200))
+TRAIN_NNZ_CAP = 30_000_000
+
+
+def _bernoulli_rows(rng, n, d, chunk=512):
+    rows, cols = [], []
+    for r0 in range(0, n, chunk):
+        r1 = min(n, r0 + chunk)
+        m = rng.random((r1 - r0, n)) < d
+        rr, cc = np.nonzero(m)
+        rows.append((rr + r0).astype(np.int32))
+        cols.append(cc.astype(np.int32))
+    return np.concatenate(rows), np.concatenate(cols)
+
+
+def training_matrix(i: int):
+    """Training matrix i (0..299) of the random 0/1 recipe: (n, row, col, val, meta)."""
+    rng = _rng(50_000 + i)
+    n = TRAIN_SIZES[i % len(TRAIN_SIZES)]
+    d = float(np.exp(rng.uniform(np.log(1e-3), np.log(0.7))))
+    d = min(d, TRAIN_NNZ_CAP / float(n * n))
+    if d > 0.02:
+        row, col = _bernoulli_rows(rng, n, d)
+    else:
+        k = int(rng.binomial(n * n, d))
+        keys = np.unique(rng.integers(0, n * n, size=k, dtype=np.int64))
+        row, col = (keys // n).astype(np.int32), (keys % n).astype(np.int32)
+    if row.size == 0:
+        row, col = np.zeros(1, np.int32), np.zeros(1, np.int32)
+    return n, row, col, np.ones(row.size, np.float32), dict(kind="random01", density=d)
+
+
+def structured_matrix(i: int):
+    """Structured training matrix i (0..119): banded, community-block,
+    power-law and grid patterns at 10^4..2x10^5 rows, values 1."""
+    rng = _rng(60_000 + i)
+    kind = ("banded", "blocks", "powerlaw", "grid")[i % 4]
+    n = int(np.exp(rng.uniform(np.log(1e4), np.log(2e5))))
+    if kind == "banded":
+        nd = int(rng.integers(1, 40))
+        offs = np.unique(rng.integers(-n // 8, n // 8, size=nd))
+        keys = []
+        for o in offs:
+            r = np.arange(max(0, -o), min(n, n - o), dtype=np.int64)
+            keep = rng.random(r.size) < rng.uniform(0.6, 1.0)
+            keys.append(r[keep] * n + r[keep] + o)
+        row, col = _canon_from_keys(np.concatenate(keys), n)
+    elif kind == "blocks":
+        size = int(rng.choice([4, 8, 16, 32]))
+        nc = max(1, n // size)
+        n = nc * size
+        p = rng.uniform(0.2, 1.0)
+        li, lj = np.triu_indices(size, k=0)
+        keep = rng.random((nc, li.size)) < p
+        base = (np.arange(nc, dtype=np.int64) * size)[:, None]
+        u = (base + li[None, :])[keep]
+        v = (base + lj[None, :])[keep]
+        inter = int(rng.integers(0, 6))
+        src = np.repeat(np.arange(n, dtype=np.int64), inter)
+        dst = rng.integers(0, n, size=src.size, dtype=np.int64)
+        row, col = _sym_with_self(np.concatenate([u, src]), np.concatenate([v, dst]), n)
+    elif kind == "powerlaw":
+        gamma = rng.uniform(1.8, 3.0)
+        deg = rng.uniform(3, 30)
+        u, v = _chung_lu_pairs(rng, n, gamma, deg, int(np.sqrt(n * deg)))
+        row, col = _sym_with_self(u, v, n)
+    else:
+        m = int(np.sqrt(n))
+        n = m * m
+        ids = np.arange(n, dtype=np.int64)
+        r, c = ids // m, ids % m
+        parts = [ids * n + ids]
+        for dr, dc in ((-1, 0), (1, 0), (0, -1), (0, 1), (-1, -1), (1, 1))[: int(rng.integers(2, 7))]:
+            ok = (r + dr >= 0) & (r + dr < m) & (c + dc >= 0) & (c + dc < m)
+            parts.append(ids[ok] * n + (ids[ok] + dr * m + dc))
+        row, col = _canon_from_keys(np.concatenate(parts), n)
+    return n, row, col, np.ones(row.size, np.float32), dict(kind=kind)

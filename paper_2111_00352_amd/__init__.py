@@ -320,7 +320,16 @@ class SelectContext:
 
     def __init__(self, mode: str = "model", fixed: str = "csr", model_path: str | None = None,
                  max_bytes: int | None = None, bsr_block: int = 16, profile_reps: int = 3):
+        """model_path None: the trained ensemble shipped in selector/model.gsm
+        (the library's hand-set trees if that file is absent); "builtin": the
+        hand-set trees."""
         _require_gpu()
+        if model_path is None:
+            from paper_2111_00352_amd.selector import MODEL_PATH
+
+            model_path = MODEL_PATH if os.path.exists(MODEL_PATH) else None
+        elif model_path == "builtin":
+            model_path = None
         self._model_path = model_path.encode() if model_path else None
         o = _SelOpts(SEL_MODES[mode], FORMATS[fixed], self._model_path, int(max_bytes or 0),
                      int(bsr_block), int(profile_reps))

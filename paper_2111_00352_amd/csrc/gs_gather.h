@@ -10,6 +10,19 @@
 
 namespace gs {
 
+// Gathered X rows: plain cached loads (GS_X_LOAD_POLICY selects an
+// alternative cache policy when the library is built for experiments).
+__device__ __forceinline__ float4 load_x4(const float *p)
+{
+#if defined(GS_X_LOAD_POLICY) && GS_X_LOAD_POLICY == 1
+    typedef float f4v __attribute__((ext_vector_type(4)));
+    const f4v v = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(p));
+    return make_float4(v[0], v[1], v[2], v[3]);
+#else
+    return *reinterpret_cast<const float4 *>(p);
+#endif
+}
+
 // One batch of B entries j .. j+B-1 of the group's current index batch:
 // B X-row loads issued back to back, then B fused multiply-adds.  MASKED
 // batches may run past the last entry m: those slots gather a valid row
@@ -28,8 +41,7 @@ __device__ __forceinline__ void gather_batch(int cj, float vj, int j, int m,
         const float *xp = X + (int64_t)cu * ldx + c0;
 #pragma unroll
         for (int q = 0; q < NQ; q++)
-            x[u][q] = qok[q] ? *reinterpret_cast<const float4 *>(xp + 4 * G * q)
-                             : make_float4(0.f, 0.f, 0.f, 0.f);
+            x[u][q] = qok[q] ? load_x4(xp + 4 * G * q) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 #pragma unroll
     for (int u = 0; u < B; u++) {

@@ -152,13 +152,15 @@ void model_input(const gs_features &f, int64_t F, double *x)
     x[20] = (double)F;
 }
 
-// Min-max scaling to [0,1] with the training range, clipped (Sec. 4.4).
+// Min-max scaling to [0,1] with the training range, clipped (Sec. 4.4), then
+// rounded to fp32: tree thresholds are learned on fp32 features.
 void normalise(const Model &m, double *x)
 {
     for (int i = 0; i < kNFeat; i++) {
         const double span = m.mx[i] - m.mn[i];
         double v = span > 0 ? (x[i] - m.mn[i]) / span : 0.0;
-        x[i] = v < 0 ? 0 : (v > 1 ? 1 : v);
+        v = v < 0 ? 0 : (v > 1 ? 1 : v);
+        x[i] = (double)(float)v;
     }
 }
 

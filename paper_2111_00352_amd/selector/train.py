@@ -1,0 +1,178 @@
+"""Train the format predictor from profiled data and export it.
+
+Usage: python -m paper_2111_00352_amd.selector.train [DATA.csv] [--out model.gsm]
+
+Labels follow Eq. 1 with w = 1: the fastest format of each (matrix, F) row,
+formats within 1% counting as tied and resolved in the order CSR < COO < ELL
+< DIA < BSR (the library's profiling selector uses the same rule).  Features
+(F1..F19 of Table 2, the 16x16 block fill, F) are min-max scaled to [0,1]
+with the training range and clipped (Sec. 4.4), then rounded to fp32.  The
+classifier is scikit-learn's gradient-boosted trees (xgboost is not
+available); the ensemble is exported as per-class score trees and checked to
+predict exactly as scikit-learn does.  Evaluation is grouped k-fold cross-
+validation: a matrix is never in both the training and the test fold.
+"""
+import argparse
+import csv
+import math
+import os
+import sys
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, os.path.dirname(os.path.dirname(HERE)))
+
+from paper_2111_00352_amd.selector import DATA_PATH, MODEL_PATH  # noqa: E402
+
+FMT_IDS = {"coo": 0, "csr": 1, "ell": 2, "dia": 3, "bsr": 4}
+TIE_ORDER = ["csr", "coo", "ell", "dia", "bsr"]
+FEATS = ["numRow", "numCol", "NNZ", "N_diags", "aver_RD", "max_RD", "min_RD", "dev_RD",
+         "aver_CD", "max_CD", "min_CD", "dev_CD", "ER_DIA", "ER_CD", "row_bounce",
+         "col_bounce", "density", "cv", "max_mu"]
+
+
+def load(path):
+    with open(path) as fh:
+        rows = list(csv.DictReader(fh))
+    X, T, groups, kinds = [], [], [], []
+    for r in rows:
+        nb = float(r["n_blocks16"])
+        x = [float(r[f]) for f in FEATS]
+        x.append(float(r["NNZ"]) / (256.0 * nb) if nb > 0 else 0.0)
+        x.append(float(r["F"]))
+        X.append(x)
+        T.append([float(r[f"t_{f}"]) for f in TIE_ORDER])
+        groups.append(f"{r['set']}:{r['index']}")
+        kinds.append(r["kind"])
+    return np.array(X), np.array(T), np.array(groups), np.array(kinds)
+
+
+def labels(T):
+    out = []
+    for t in T:
+        best = min(t)
+        out.append(next(i for i, v in enumerate(t) if v <= best * 1.01))
+    return np.array(out)  # index into TIE_ORDER
+
+
+def normalise(X, mn, mx):
+    span = mx - mn
+    Z = np.where(span > 0, (X - mn) / np.where(span > 0, span, 1), 0.0)
+    return np.clip(Z, 0, 1).astype(np.float32).astype(np.float64)
+
+
+def fit(Xn, y, seed=0):
+    from sklearn.ensemble import GradientBoostingClassifier
+
+    clf = GradientBoostingClassifier(n_estimators=80, max_depth=3, learning_rate=0.2,
+                                     subsample=1.0, random_state=seed)
+    clf.fit(Xn, y)
+    return clf
+
+
+def export(clf, mn, mx, path):
+    classes = list(clf.classes_)
+    K = len(classes)
+    lr = clf.learning_rate
+    base = clf._raw_predict_init(np.zeros((1, mn.size)))[0]
+    trees = []
+    est = clf.estimators_
+    for stage in est:
+        for k, tree in enumerate(stage):
+            cls = k if K > 2 else 1
+            t = tree.tree_
+            nodes = []
+            for i in range(t.node_count):
+                if t.children_left[i] == -1:
+                    nodes.append((-1, 0.0, 0, 0, lr * float(t.value[i][0][0])))
+                else:
+                    thr = float(np.nextafter(t.threshold[i], np.inf))  # x <= thr  ->  x < next(thr)
+                    nodes.append((int(t.feature[i]), thr, int(t.children_left[i]),
+                                  int(t.children_right[i]), 0.0))
+            trees.append((cls, nodes))
+    if K > 2:
+        base_scores = list(base)
+    else:
+        base_scores = [0.0, float(base[0])]
+    lines = ["GSMODEL 1", f"nfeat {mn.size}",
+             "classes %d %s" % (K, " ".join(str(FMT_IDS[TIE_ORDER[c]]) for c in classes)),
+             "min " + " ".join(repr(float(v)) for v in mn),
+             "max " + " ".join(repr(float(v)) for v in mx),
+             "base " + " ".join(repr(float(v)) for v in base_scores),
+             f"ntrees {len(trees)}"]
+    for cls, nodes in trees:
+        lines.append(f"tree {cls} {len(nodes)}")
+        for f, thr, l, r, v in nodes:
+            lines.append(f"{f} {thr!r} {l} {r} {v!r}")
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    return trees, base_scores, classes
+
+
+def score_exported(trees, base_scores, Xn):
+    S = np.tile(np.array(base_scores, dtype=np.float64), (Xn.shape[0], 1))
+    for cls, nodes in trees:
+        for r in range(Xn.shape[0]):
+            i = 0
+            while nodes[i][0] >= 0:
+                f, thr, l, rr, _ = nodes[i]
+                i = l if Xn[r, f] < thr else rr
+            S[r, cls] += nodes[i][4]
+    return S
+
+
+def evaluate(T, pred):
+    """Geometric-mean speedup over fixed CSR and fraction of the oracle."""
+    tc = T[:, 0]
+    tbest = T.min(axis=1)
+    tsel = T[np.arange(len(pred)), pred]
+    ok = np.isfinite(tsel)
+    sp = np.exp(np.mean(np.log(tc[ok] / tsel[ok])))
+    frac = np.exp(np.mean(np.log(tbest[ok] / tsel[ok])))
+    orac = np.exp(np.mean(np.log(tc / tbest)))
+    return sp, frac, orac, int((~ok).sum())
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("data", nargs="?", default=DATA_PATH)
+    ap.add_argument("--out", default=MODEL_PATH)
+    ap.add_argument("--folds", type=int, default=5)
+    a = ap.parse_args()
+    from sklearn.model_selection import GroupKFold
+
+    X, T, groups, kinds = load(a.data)
+    y = labels(T)
+    print(f"{len(y)} samples, {len(set(groups))} matrices; label counts: "
+          + ", ".join(f"{TIE_ORDER[c]}={int((y == c).sum())}" for c in range(5)))
+    # cross-validation on unseen matrices
+    pred = np.zeros_like(y)
+    for tr, te in GroupKFold(n_splits=a.folds).split(X, y, groups):
+        mn, mx = X[tr].min(axis=0), X[tr].max(axis=0)
+        clf = fit(normalise(X[tr], mn, mx), y[tr])
+        pred[te] = clf.predict(normalise(X[te], mn, mx))
+    acc = float((pred == y).mean())
+    sp, frac, orac, bad = evaluate(T, pred)
+    print(f"cross-validated accuracy {acc:.3f}; speedup over CSR {sp:.3f}x (oracle {orac:.3f}x); "
+          f"fraction of oracle performance {frac:.3f}; infeasible picks {bad}")
+    for kd in sorted(set(kinds)):
+        m = kinds == kd
+        s2, f2, o2, _ = evaluate(T[m], pred[m])
+        print(f"  {kd:10s} n={int(m.sum()):4d} acc {float((pred[m] == y[m]).mean()):.3f} "
+              f"speedup {s2:.3f}x oracle {o2:.3f}x fraction {f2:.3f}")
+    # final model on everything
+    mn, mx = X.min(axis=0), X.max(axis=0)
+    Xn = normalise(X, mn, mx)
+    clf = fit(Xn, y)
+    trees, base, classes = export(clf, mn, mx, a.out)
+    S = score_exported(trees, base, Xn)
+    ours = np.array([classes[i] for i in np.argmax(S, axis=1)])
+    agree = float((ours == clf.predict(Xn)).mean())
+    print(f"exported {len(trees)} trees to {a.out}; agreement with scikit-learn {agree:.4f}")
+    if agree < 1.0:
+        sys.exit("exported model disagrees with scikit-learn")
+
+
+if __name__ == "__main__":
+    main()

@@ -356,5 +356,21 @@ def test_select_and_run_modes(mode):
 def test_select_model_on_mesh_prefers_diagonals():
     g = graphgen.scaled(3)
     case = _case_from_graph(g)
-    ctx = gs.SelectContext("model")
+    ctx = gs.SelectContext("model", model_path="builtin")  # the hand-set trees
     assert ctx.select(1, case.d_row, case.d_col, case.d_val, (case.R, case.C), 64) == "dia"
+
+
+def test_trained_model_choice_is_near_the_profiled_best():
+    # the shipped ensemble against the exhaustive selector on unseen inputs
+    ratios = []
+    for k in (2, 3, 4):
+        g = graphgen.scaled(k)
+        case = _case_from_graph(g)
+        X = _dev(g.X)
+        shape = (case.R, case.C)
+        prof = gs.SelectContext("profile", profile_reps=5)
+        prof.run(1, case.d_row, case.d_col, case.d_val, shape, X)
+        times = {f: t for f, t in prof.stats()["scores"].items() if t > 0}
+        chosen = gs.SelectContext("model").select(1, case.d_row, case.d_col, case.d_val, shape, g.F)
+        ratios.append(min(times.values()) / times[chosen])
+    assert np.exp(np.mean(np.log(ratios))) > 0.6, ratios

@@ -120,3 +120,26 @@ def test_allocator_hooks_must_be_paired(L):
     a = gs._Allocator(gs._ALLOC_FN(lambda n, s, c: None), gs._FREE_FN(), None)
     assert L.gs_set_allocator(ctypes.byref(a)) == gs.ERR_INVALID_ARG
     assert L.gs_set_allocator(None) == 0
+
+
+def test_shipped_trained_model_parses(L):
+    from paper_2111_00352_amd.selector import MODEL_PATH
+    assert os.path.exists(MODEL_PATH)
+    rc, h = _ctx(L, path=MODEL_PATH.encode())
+    assert rc == 0, L.gs_last_error()
+    L.gs_ctx_destroy(h)
+
+
+def test_trained_model_export_matches_sklearn(tmp_path):
+    # re-train on the shipped profile data and check the exported trees
+    # predict exactly what scikit-learn predicts (the library walks them)
+    import numpy as np
+    from paper_2111_00352_amd.selector import DATA_PATH, train
+    X, T, groups, kinds = train.load(DATA_PATH)
+    y = train.labels(T)
+    mn, mx = X.min(axis=0), X.max(axis=0)
+    Xn = train.normalise(X, mn, mx)
+    clf = train.fit(Xn, y)
+    trees, base, classes = train.export(clf, mn, mx, str(tmp_path / "m.gsm"))
+    S = train.score_exported(trees, base, Xn)
+    assert (np.array([classes[i] for i in S.argmax(axis=1)]) == clf.predict(Xn)).all()
