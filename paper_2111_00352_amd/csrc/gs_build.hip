@@ -6,6 +6,7 @@
 // differs from the one already held (Sec. 4).  Index work only: values are
 // moved, never computed, so every output is bit-exact and deterministic.
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 
 #include "gs_device.h"
@@ -262,7 +263,11 @@ __global__ __launch_bounds__(kTB) void k_dia_mark(const int32_t *__restrict__ ro
     for (int64_t k = (int64_t)blockIdx.x * kTB + threadIdx.x; k < Z;
          k += (int64_t)gridDim.x * kTB) {
         int64_t sidx = (int64_t)col[k] - row[k] + R - 1;
-        atomicOr(&bm[sidx >> 5], 1u << (sidx & 31));
+        // bits only ever get set: skip the atomic when the word already has it
+        // (the main diagonal alone gets one hit per row)
+        const uint32_t bit = 1u << (sidx & 31);
+        if (!(__hip_atomic_load(&bm[sidx >> 5], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit))
+            atomicOr(&bm[sidx >> 5], bit);
     }
 }
 
@@ -377,6 +382,41 @@ __global__ __launch_bounds__(kTB) void k_bsr_count(const int32_t *__restrict__ r
     if (lane == 0) cnt[br] = n;
 }
 
+// Block count with a bitmap of block columns in LDS (nbc bits), one
+// workgroup per block row (persistent): the block row's entries are one
+// contiguous range of col[], each marks its block column, the count is the
+// bitmap's population.
+__global__ __launch_bounds__(kTB) void k_bsr_count_lds(const int32_t *__restrict__ rp,
+                                                       const int32_t *__restrict__ col, int64_t R,
+                                                       int b, int64_t nbr, int64_t nw,
+                                                       int32_t *__restrict__ cnt)
+{
+    extern __shared__ uint32_t bmp[];
+    __shared__ int wsum[kTB / kWave];
+    for (int64_t br = blockIdx.x; br < nbr; br += gridDim.x) {
+        for (int64_t w = threadIdx.x; w < nw; w += kTB) bmp[w] = 0u;
+        __syncthreads();
+        const int64_t r1 = (br + 1) * b < R ? (br + 1) * b : R;
+        const int64_t k0 = rp[br * b], k1 = rp[r1];
+        for (int64_t kk = k0 + threadIdx.x; kk < k1; kk += kTB) {
+            const uint32_t c = (uint32_t)(col[kk] / b);
+            atomicOr(&bmp[c >> 5], 1u << (c & 31));
+        }
+        __syncthreads();
+        int n = 0;
+        for (int64_t w = threadIdx.x; w < nw; w += kTB) n += __popc(bmp[w]);
+        n = wave_sum_i32(n);
+        if (lane_id() == 0) wsum[threadIdx.x / kWave] = n;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int t = 0;
+            for (int i = 0; i < kTB / kWave; i++) t += wsum[i];
+            cnt[br] = t;
+        }
+        __syncthreads();
+    }
+}
+
 __global__ __launch_bounds__(kTB) void k_bsr_fill(const int32_t *__restrict__ rp,
                                                   const int32_t *__restrict__ col,
                                                   const float *__restrict__ val, int64_t R, int b,
@@ -475,6 +515,22 @@ __global__ __launch_bounds__(kTB) void k_expand_rows(const int32_t *__restrict__
         for (int64_t k = rp[i]; k < rp[i + 1]; k++) orow[k] = (int32_t)i;
 }
 
+
+// Distinct (row/b, col/b) blocks per block row into cnt[0..nbr).  The LDS
+// bitmap kernel needs nbc/8 bytes of LDS; wider matrices use the merge.
+void launch_block_count(const int32_t *rp, const int32_t *col, int64_t R, int64_t C, int b,
+                        int64_t nbr, int32_t *cnt, hipStream_t s)
+{
+    const int64_t nbc = ceil_div(C, b), nw = ceil_div(nbc, 32);
+    const char *force_merge = std::getenv("GS_BLOCK_COUNT_MERGE");
+    if (nw * 4 <= 48 * 1024 && !(force_merge && *force_merge == '1')) {
+        const int64_t g = std::min<int64_t>(nbr, 256 * 8);
+        k_bsr_count_lds<<<(unsigned)std::max<int64_t>(1, g), kTB, (size_t)nw * 4, s>>>(rp, col, R, b, nbr, nw, cnt);
+    } else {
+        k_bsr_count<<<grid_for(nbr * kWave), kTB, 0, s>>>(rp, col, R, b, nbr, cnt);
+    }
+    GS_LAUNCH_CHECK();
+}
 
 int read_flag(const int *d_flags, hipStream_t s)
 {
@@ -611,10 +667,8 @@ int64_t count_blocks(const gs_matrix_ &csr, int b, hipStream_t s)
     if (nbr == 0 || csr.Z == 0) return 0;
     DevBuf cnt;
     cnt.alloc((size_t)(nbr + 1) * 4, s);
-    k_bsr_count<<<grid_for(nbr * kWave), kTB, 0, s>>>(csr.row_ptr.as<int32_t>(),
-                                                      csr.col.as<int32_t>(), csr.R, b, nbr,
-                                                      cnt.as<int32_t>());
-    GS_LAUNCH_CHECK();
+    launch_block_count(csr.row_ptr.as<int32_t>(), csr.col.as<int32_t>(), csr.R, csr.C, b, nbr,
+                       cnt.as<int32_t>(), s);
     exclusive_scan_i32(cnt.as<int32_t>(), cnt.as<int32_t>(), nbr, true, s);
     int32_t nb = 0;
     GS_HIP(hipMemcpyAsync(&nb, cnt.as<int32_t>() + nbr, 4, hipMemcpyDeviceToHost, s));
@@ -742,10 +796,7 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
             const int64_t nbr = ceil_div(R, b);
             DevBuf cnt;
             cnt.alloc((size_t)(nbr + 1) * 4, s);
-            if (nbr) {
-                k_bsr_count<<<grid_for(nbr * kWave), kTB, 0, s>>>(rp, col, R, b, nbr, cnt.as<int32_t>());
-                GS_LAUNCH_CHECK();
-            }
+            if (nbr) launch_block_count(rp, col, R, C, b, nbr, cnt.as<int32_t>(), s);
             exclusive_scan_i32(cnt.as<int32_t>(), cnt.as<int32_t>(), nbr, true, s);
             int32_t nb = 0;
             GS_HIP(hipMemcpyAsync(&nb, cnt.as<int32_t>() + nbr, 4, hipMemcpyDeviceToHost, s));

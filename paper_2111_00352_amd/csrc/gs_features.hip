@@ -85,7 +85,11 @@ __global__ __launch_bounds__(kTB) void k_mark_diags(const int32_t *__restrict__ 
     for (int64_t i = ((int64_t)blockIdx.x * kTB + threadIdx.x) / kWave; i < R; i += waves) {
         for (int64_t k = rp[i] + lane; k < rp[i + 1]; k += kWave) {
             int64_t sidx = (int64_t)col[k] - i + R - 1;
-            atomicOr(&bm[sidx >> 5], 1u << (sidx & 31));
+            // bits only ever get set: skip the atomic when the word already has it
+            // (the main diagonal alone gets one hit per row)
+            const uint32_t bit = 1u << (sidx & 31);
+            if (!(__hip_atomic_load(&bm[sidx >> 5], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit))
+                atomicOr(&bm[sidx >> 5], bit);
         }
     }
 }

@@ -115,6 +115,9 @@ struct gs_matrix_ {
     gs::DevBuf long_first;   // int32 [n_long_rows+1] -> first partial slot of each long row
     gs::DevBuf csr_items;    // int4 {row, start, len, slot} work items
     int64_t n_items = 0;
+    int64_t n_short = 0;     // short items (after the n_long_chunks chunk items)
+    int64_t n_medium_rows = 0, n_medium_chunks = 0;  // long rows of at most csr_wg_thr entries
+    int csr_wg_thr = 0;
     bool csr_sorted = false; // items ordered by decreasing length
     // COO: rows with no entries (zeroed by the COO kernel)
     int64_t n_empty_rows = 0;
@@ -135,6 +138,9 @@ constexpr int kDefaultBsrBlock = 16;
 constexpr int kCsrLongRow = 128;
 // Chunk length of the split CSR path and of the COO segmented reduction.
 constexpr int kCsrChunk = 128;
+// Long rows up to this many entries take one workgroup on the vectorised
+// path; longer ones are split across workgroups.
+constexpr int kCsrWgRow = 1024;
 constexpr int kCooChunk = 128;
 // A 16x16 BSR block with at least this many stored columns counts as dense.
 constexpr int kBsrDenseCols = 8;

@@ -275,23 +275,14 @@ def test_convert_between_formats(src):
     assert f["f"] == fo.tolist()
 
 
-@pytest.mark.parametrize("xs", [1, 2, 4, 8])
+@pytest.mark.parametrize("cpl", [4, 8, 16])
+@pytest.mark.parametrize("sort", [1, 2])
 @pytest.mark.parametrize("F", [64, 128, 256])
-def test_csr_xcd_slicing(monkeypatch, xs, F):
-    # the CSR kernel can pin column slices of F to XCDs; every split must agree
-    monkeypatch.setenv("GS_CSR_XSLICE", str(xs))
-    g = graphgen.scaled(2)
-    case = _case_from_graph(g)
-    X = graphgen.features_x(case.C, F, 40 + F, "normal")
-    check_spmm(case, case.build("csr"), X)
-
-
-@pytest.mark.parametrize("cpl,lif", [(4, 8), (8, 16), (16, 8), (16, 16)])
-@pytest.mark.parametrize("F", [64, 128, 256])
-def test_csr_lane_shapes(monkeypatch, cpl, lif, F):
-    # columns per lane and loads in flight are tunable; every shape must agree
+def test_csr_lane_shapes(monkeypatch, cpl, sort, F):
+    # columns per lane and row ordering are tunable; every shape must agree,
+    # with long rows (workgroup-wide path) present in both orders
     monkeypatch.setenv("GS_CSR_CPL", str(cpl))
-    monkeypatch.setenv("GS_CSR_LIF", str(lif))
+    monkeypatch.setenv("GS_CSR_SORT", str(sort))
     g = graphgen.scaled(2)
     case = _case_from_graph(g)
     X = graphgen.features_x(case.C, F, 50 + F, "normal")
@@ -374,3 +365,18 @@ def test_trained_model_choice_is_near_the_profiled_best():
         chosen = gs.SelectContext("model").select(1, case.d_row, case.d_col, case.d_val, shape, g.F)
         ratios.append(min(times.values()) / times[chosen])
     assert np.exp(np.mean(np.log(ratios))) > 0.6, ratios
+
+
+@pytest.mark.parametrize("merge", ["0", "1"])
+def test_block_count_kernels_agree(monkeypatch, merge):
+    # the 16x16 block count (features, BSR sizing) has an LDS-bitmap kernel and
+    # a merge kernel for very wide matrices; both must give the oracle's count
+    monkeypatch.setenv("GS_BLOCK_COUNT_MERGE", merge)
+    for k in (2, 4):
+        case = _case_from_graph(graphgen.scaled(k))
+        check_features(case)
+        check_layout(case, "bsr", 16)
+    case = _random_case(777, 3001, 20000, 71)
+    check_features(case)
+    for b in (3, 16, 64):
+        check_layout(case, "bsr", b)
