@@ -122,6 +122,10 @@ struct gs_matrix_ {
     // COO: rows with no entries (zeroed by the COO kernel)
     int64_t n_empty_rows = 0;
     gs::DevBuf empty_rows;
+    // COO: chunk boundaries (row-aligned unless a row is longer than a chunk)
+    // and the chunks where a split row starts
+    int64_t n_coo_chunks = 0, n_coo_starts = 0;
+    gs::DevBuf coo_bounds, coo_starts;
 
     // F-dependent workspace (partials / carries), grown on demand.
     gs::DevBuf work;

@@ -185,7 +185,7 @@ __global__ __launch_bounds__(kBlock) void k_coo_main(int64_t Z, const int32_t *_
                                                      const float *__restrict__ val,
                                                      const float *__restrict__ X, int64_t ldx,
                                                      float *__restrict__ Y, int64_t ldy, int64_t F,
-                                                     int chunk_len, int64_t n_chunks,
+                                                     const int32_t *__restrict__ bounds, int64_t n_chunks,
                                                      float *__restrict__ work)
 {
     constexpr int GPB = kBlock / G;
@@ -194,8 +194,7 @@ __global__ __launch_bounds__(kBlock) void k_coo_main(int64_t Z, const int32_t *_
     const bool active = c0 < F;
     const int64_t q = xcd_tile(blockIdx.x, gridDim.x) * GPB + g;
     if (q >= n_chunks) return;
-    const int64_t k0 = q * chunk_len;
-    const int64_t k1 = (k0 + chunk_len < Z) ? k0 + chunk_len : Z;
+    const int64_t k0 = bounds[q], k1 = bounds[q + 1];
     const bool head_cont = k0 > 0 && row[k0 - 1] == row[k0];
     const bool tail_cont = k1 < Z && row[k1] == row[k1 - 1];
     const int gbase = (threadIdx.x % kWave) / G * G;  // first lane of this group in the wave
@@ -254,13 +253,16 @@ __global__ __launch_bounds__(kBlock) void k_coo_main(int64_t Z, const int32_t *_
                    active);
 }
 
-// Groups [0, n_chunks): chunk q whose last segment starts a spanning row
-// adds that row's carries (slot T of q, then slot H of q+1, q+2, ... while
-// the row continues) and writes Y.  Groups after that zero the empty rows.
+// Groups [0, n_starts): chunk starts[e], whose last segment begins a row
+// that runs on into later chunks, adds that row's carries (slot T of its
+// chunk, then slot H of the following chunks while the row continues) and
+// writes Y.  Groups after that zero the empty rows.
 template <int VEC, int G>
 __global__ __launch_bounds__(kBlock) void k_coo_fixup(int64_t Z, const int32_t *__restrict__ row,
-                                                      int chunk_len, int64_t n_chunks,
-                                                      const float *__restrict__ work,
+                                                      const int32_t *__restrict__ bounds,
+                                                      int64_t n_chunks,
+                                                      const int32_t *__restrict__ starts,
+                                                      int64_t n_starts, const float *__restrict__ work,
                                                       const int32_t *__restrict__ empty_rows,
                                                       int64_t n_empty, float *__restrict__ Y,
                                                       int64_t ldy, int64_t F)
@@ -268,16 +270,11 @@ __global__ __launch_bounds__(kBlock) void k_coo_fixup(int64_t Z, const int32_t *
     constexpr int GPB = kBlock / G;
     const int g = threadIdx.x / G, lane = threadIdx.x % G;
     const int64_t c0 = (int64_t)blockIdx.y * (G * VEC) + (int64_t)lane * VEC;
-    const int64_t q = (int64_t)blockIdx.x * GPB + g;
+    const int64_t e = (int64_t)blockIdx.x * GPB + g;
     if (c0 >= F) return;
-    if (q < n_chunks) {
-        const int64_t k0 = q * chunk_len;
-        const int64_t k1 = (k0 + chunk_len < Z) ? k0 + chunk_len : Z;
-        const bool tail_cont = k1 < Z && row[k1] == row[k1 - 1];
-        if (!tail_cont) return;
-        const bool head_cont = k0 > 0 && row[k0 - 1] == row[k0];
-        const int32_t r = row[k1 - 1];
-        if (head_cont && row[k0] == r) return;  // the row started in an earlier chunk
+    if (e < n_starts) {
+        const int64_t q = starts[e];
+        const int32_t r = row[bounds[q + 1] - 1];
         Acc<VEC> acc;
         acc.zero();
         const Vec<VEC> t = ld_vec<VEC>(work + (q * 2 + 1) * F + c0);
@@ -287,19 +284,18 @@ __global__ __launch_bounds__(kBlock) void k_coo_fixup(int64_t Z, const int32_t *
             const Vec<VEC> h = ld_vec<VEC>(work + (p * 2 + 0) * F + c0);
 #pragma unroll
             for (int i = 0; i < VEC; i++) acc.v[i] += h.v[i];
-            const int64_t p0 = p * chunk_len;
-            const int64_t p1 = (p0 + chunk_len < Z) ? p0 + chunk_len : Z;
+            const int64_t p1 = bounds[p + 1];
             const bool whole = row[p1 - 1] == r && p1 < Z && row[p1] == r;
             if (!whole) break;
         }
         st_vec_stream<VEC>(Y + (int64_t)r * ldy + c0, acc.vec());
     } else {
-        const int64_t e = q - n_chunks;
-        if (e >= n_empty) return;
+        const int64_t k = e - n_starts;
+        if (k >= n_empty) return;
         Vec<VEC> z;
 #pragma unroll
         for (int i = 0; i < VEC; i++) z.v[i] = 0.0f;
-        st_vec_stream<VEC>(Y + (int64_t)empty_rows[e] * ldy + c0, z);
+        st_vec_stream<VEC>(Y + (int64_t)empty_rows[k] * ldy + c0, z);
     }
 }
 
@@ -504,21 +500,52 @@ int env_int_coo(const char *name, int dflt)
 
 // --------------------------------------------------------------- plans
 
+// COO chunks follow row boundaries: whole rows are packed into chunks of at
+// most `chunk` entries, and only a row longer than that is cut into chunk-
+// sized pieces (whose partial sums the fixup launch adds).  Also lists the
+// empty rows, which the kernel must zero.
 void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s)
 {
-    m.coo_chunk = env_int_coo("GS_COO_CHUNK", kCooChunk);
+    const int chunk = env_int_coo("GS_COO_CHUNK", kCooChunk);
+    m.coo_chunk = chunk;
     std::vector<int32_t> rp((size_t)m.R + 1);
     GS_HIP(hipMemcpyAsync(rp.data(), row_ptr, rp.size() * 4, hipMemcpyDeviceToHost, s));
     GS_HIP(hipStreamSynchronize(s));
-    std::vector<int32_t> empty;
-    for (int64_t i = 0; i < m.R; i++)
-        if (rp[i + 1] == rp[i]) empty.push_back((int32_t)i);
-    m.n_empty_rows = (int64_t)empty.size();
-    m.empty_rows.alloc(empty.size() * 4, s);
-    if (!empty.empty()) {
-        GS_HIP(hipMemcpyAsync(m.empty_rows.p, empty.data(), empty.size() * 4, hipMemcpyHostToDevice, s));
-        GS_HIP(hipStreamSynchronize(s));
+    std::vector<int32_t> empty, bounds{0}, starts;
+    int64_t cur = 0;
+    for (int64_t i = 0; i < m.R; i++) {
+        const int32_t pos = rp[i], len = rp[i + 1] - rp[i];
+        if (len == 0) {
+            empty.push_back((int32_t)i);
+            continue;
+        }
+        if (len > chunk) {
+            if (pos > bounds.back()) bounds.push_back(pos);
+            starts.push_back((int32_t)bounds.size() - 1);
+            for (int32_t o = chunk; o < len; o += chunk) bounds.push_back(pos + o);
+            bounds.push_back(pos + len);
+            cur = 0;
+            continue;
+        }
+        if (cur + len > chunk) {
+            bounds.push_back(pos);
+            cur = 0;
+        }
+        cur += len;
     }
+    if (m.Z > bounds.back()) bounds.push_back((int32_t)m.Z);
+    m.n_coo_chunks = (int64_t)bounds.size() - 1;
+    m.n_coo_starts = (int64_t)starts.size();
+    m.n_empty_rows = (int64_t)empty.size();
+    m.coo_bounds.alloc(bounds.size() * 4, s);
+    m.coo_starts.alloc(starts.size() * 4, s);
+    m.empty_rows.alloc(empty.size() * 4, s);
+    GS_HIP(hipMemcpyAsync(m.coo_bounds.p, bounds.data(), bounds.size() * 4, hipMemcpyHostToDevice, s));
+    if (!starts.empty())
+        GS_HIP(hipMemcpyAsync(m.coo_starts.p, starts.data(), starts.size() * 4, hipMemcpyHostToDevice, s));
+    if (!empty.empty())
+        GS_HIP(hipMemcpyAsync(m.empty_rows.p, empty.data(), empty.size() * 4, hipMemcpyHostToDevice, s));
+    GS_HIP(hipStreamSynchronize(s));
 }
 
 // --------------------------------------------------------------- launchers
@@ -552,22 +579,23 @@ void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
               hipStream_t s)
 {
     const Shape sh = pick_shape(X, ldx, Y, ldy, F);
-    const int chunk = m.coo_chunk;
-    const int64_t n_chunks = ceil_div(m.Z, chunk);
-    if (n_chunks) ensure_work(m, (size_t)n_chunks * 2 * F * 4, s);
+    const int64_t n_chunks = m.n_coo_chunks;
+    if (m.n_coo_starts) ensure_work(m, (size_t)n_chunks * 2 * F * 4, s);
     dispatch(sh, [&]<int VEC, int G>() {
         constexpr int GPB = kBlock / G;
         if (n_chunks) {
             dim3 grid(u32_grid(ceil_div(n_chunks, GPB)), (unsigned)sh.fslices);
             k_coo_main<VEC, G><<<grid, kBlock, 0, s>>>(m.Z, m.row.as<int32_t>(), m.col.as<int32_t>(),
-                                                       m.val.as<float>(), X, ldx, Y, ldy, F, chunk,
-                                                       n_chunks, m.work.as<float>());
+                                                       m.val.as<float>(), X, ldx, Y, ldy, F,
+                                                       m.coo_bounds.as<int32_t>(), n_chunks,
+                                                       m.work.as<float>());
             GS_HIP(hipGetLastError());
         }
-        const int64_t groups = n_chunks + m.n_empty_rows;
+        const int64_t groups = m.n_coo_starts + m.n_empty_rows;
         if (groups) {
             dim3 g2(u32_grid(ceil_div(groups, GPB)), (unsigned)sh.fslices);
-            k_coo_fixup<VEC, G><<<g2, kBlock, 0, s>>>(m.Z, m.row.as<int32_t>(), chunk, n_chunks,
+            k_coo_fixup<VEC, G><<<g2, kBlock, 0, s>>>(m.Z, m.row.as<int32_t>(), m.coo_bounds.as<int32_t>(),
+                                                      n_chunks, m.coo_starts.as<int32_t>(), m.n_coo_starts,
                                                       m.work.as<float>(), m.empty_rows.as<int32_t>(),
                                                       m.n_empty_rows, Y, ldy, F);
             GS_HIP(hipGetLastError());
