@@ -48,11 +48,11 @@ gs_build_opts resolve_opts(const gs_build_opts *o)
     return r;
 }
 
-gs_matrix_ *build_csr(const gs_coo *A, const gs_build_opts &o, hipStream_t s)
+gs_matrix_ *build_csr(const gs_coo *A, const gs_build_opts &o, hipStream_t s, bool plan)
 {
     CanonCOO c;
     canonicalize(*A, o.assume_canonical != 0, s, c);
-    return csr_from_canon(std::move(c), s);
+    return csr_from_canon(std::move(c), s, plan);
 }
 
 void run_spmm(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
@@ -83,7 +83,7 @@ int gs_build_format(const gs_coo *A, int fmt, const gs_build_opts *opts, gs_stre
         check_coo(A);
         const gs_build_opts o = resolve_opts(opts);
         hipStream_t s = (hipStream_t)stream;
-        gs_matrix_ *csr = build_csr(A, o, s);
+        gs_matrix_ *csr = build_csr(A, o, s, fmt == GS_CSR);
         if (fmt == GS_CSR) {
             if (bytes_required) *bytes_required = csr->device_bytes;
             *out = csr;
@@ -149,7 +149,7 @@ int gs_extract_features(const gs_coo *A, const gs_build_opts *opts, gs_stream st
         check_coo(A);
         const gs_build_opts o = resolve_opts(opts);
         hipStream_t s = (hipStream_t)stream;
-        gs_matrix_ *csr = build_csr(A, o, s);
+        gs_matrix_ *csr = build_csr(A, o, s, false);
         try {
             features_from_csr(*csr, s, out);
         } catch (...) {

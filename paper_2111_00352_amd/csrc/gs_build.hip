@@ -256,21 +256,6 @@ __global__ __launch_bounds__(kTB) void k_ell_to_coo(const int32_t *__restrict__ 
 // Diagonal d of the R x C matrix has offset col - row in [-(R-1), C-1];
 // slot index sidx = offset + R - 1.  A bitmap marks the occupied ones.
 
-__global__ __launch_bounds__(kTB) void k_dia_mark(const int32_t *__restrict__ row,
-                                                  const int32_t *__restrict__ col, int64_t Z,
-                                                  int64_t R, uint32_t *__restrict__ bm)
-{
-    for (int64_t k = (int64_t)blockIdx.x * kTB + threadIdx.x; k < Z;
-         k += (int64_t)gridDim.x * kTB) {
-        int64_t sidx = (int64_t)col[k] - row[k] + R - 1;
-        // bits only ever get set: skip the atomic when the word already has it
-        // (the main diagonal alone gets one hit per row)
-        const uint32_t bit = 1u << (sidx & 31);
-        if (!(__hip_atomic_load(&bm[sidx >> 5], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit))
-            atomicOr(&bm[sidx >> 5], bit);
-    }
-}
-
 __global__ __launch_bounds__(kTB) void k_popc_words(const uint32_t *__restrict__ bm, int64_t nw,
                                                     int32_t *__restrict__ cnt)
 {
@@ -619,7 +604,7 @@ void canonicalize(const gs_coo &A, bool assume_canonical, hipStream_t s, CanonCO
     if (f & kFlagDup) fail(GS_ERR_DUPLICATE, "COO holds duplicate (row, col) entries");
 }
 
-gs_matrix_ *csr_from_canon(CanonCOO &&c, hipStream_t s)
+gs_matrix_ *csr_from_canon(CanonCOO &&c, hipStream_t s, bool plan)
 {
     gs_matrix_ *m = new gs_matrix_();
     try {
@@ -636,7 +621,7 @@ gs_matrix_ *csr_from_canon(CanonCOO &&c, hipStream_t s)
         m->val = std::move(c.val);
         m->device_bytes = (uint64_t)(c.R + 1) * 4 + (uint64_t)c.Z * 8;
         GS_HIP(hipStreamSynchronize(s));  // c.row is released by the caller
-        plan_csr(*m, s);
+        if (plan) plan_csr(*m, s);
     } catch (...) {
         delete m;
         throw;
@@ -755,11 +740,9 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
             wpos.alloc((size_t)(nw + 1) * 4, s);
             row.alloc((size_t)Z * 4, s);
             if (Z) {
-                GS_HIP(hipMemsetAsync(bm.p, 0, (size_t)(nw + 1) * 4, s));
                 k_expand_rows<<<elem_grid(R), kTB, 0, s>>>(rp, R, row.as<int32_t>());
                 GS_LAUNCH_CHECK();
-                k_dia_mark<<<elem_grid(Z), kTB, 0, s>>>(row.as<int32_t>(), col, Z, R, bm.as<uint32_t>());
-                GS_LAUNCH_CHECK();
+                diag_bitmap(rp, col, R, C, Z, bm.as<uint32_t>(), s);
                 k_popc_words<<<elem_grid(nw), kTB, 0, s>>>(bm.as<uint32_t>(), nw, wpos.as<int32_t>());
                 GS_LAUNCH_CHECK();
                 exclusive_scan_i32(wpos.as<int32_t>(), wpos.as<int32_t>(), nw, true, s);

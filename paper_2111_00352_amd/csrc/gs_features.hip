@@ -5,8 +5,10 @@
 // the number of occupied 16x16 blocks), combined with integer atomics, so
 // the result is exact and deterministic.  The 19 doubles are then formed on
 // the host from those integers in one fixed operation order.
+#include <algorithm>
 #include <climits>
 #include <cmath>
+#include <cstdlib>
 
 #include "gs_device.h"
 #include "gs_internal.h"
@@ -38,10 +40,16 @@ __global__ __launch_bounds__(kTB) void k_col_hist(const int32_t *__restrict__ co
 }
 
 // Statistics of a count sequence cnt[i] = (ptr ? ptr[i+1]-ptr[i] : vals[i]).
+// Each workgroup reduces in registers, then across its waves in LDS, and
+// issues one set of atomics (the grid is kept small, so the few atomics on
+// the shared accumulator do not queue up).
 __global__ __launch_bounds__(kTB) void k_count_stats(const int32_t *__restrict__ ptr,
                                                      const int32_t *__restrict__ vals, int64_t n,
                                                      int is_row, FeatAcc *__restrict__ acc)
 {
+    constexpr int NWV = kTB / kWave;
+    __shared__ unsigned long long s_s2[NWV], s_bn[NWV];
+    __shared__ int s_mx[NWV], s_mn[NWV];
     unsigned long long s2 = 0, bn = 0;
     int mx = 0, mn = INT_MAX;
     for (int64_t i = (int64_t)blockIdx.x * kTB + threadIdx.x; i < n;
@@ -59,23 +67,116 @@ __global__ __launch_bounds__(kTB) void k_count_stats(const int32_t *__restrict__
     bn = wave_sum_u64(bn);
     mx = wave_max_i32(mx);
     mn = wave_min_i32(mn);
+    const int w = threadIdx.x / kWave;
     if (lane_id() == 0) {
-        if (is_row) {
-            atomicAdd(&acc->s2r, s2);
-            atomicAdd(&acc->bnr, bn);
-            atomicMax(&acc->maxr, mx);
-            atomicMin(&acc->minr, mn);
-        } else {
-            atomicAdd(&acc->s2c, s2);
-            atomicAdd(&acc->bnc, bn);
-            atomicMax(&acc->maxc, mx);
-            atomicMin(&acc->minc, mn);
-        }
+        s_s2[w] = s2;
+        s_bn[w] = bn;
+        s_mx[w] = mx;
+        s_mn[w] = mn;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    for (int v = 1; v < NWV; v++) {
+        s2 += s_s2[v];
+        bn += s_bn[v];
+        mx = s_mx[v] > mx ? s_mx[v] : mx;
+        mn = s_mn[v] < mn ? s_mn[v] : mn;
+    }
+    if (is_row) {
+        atomicAdd(&acc->s2r, s2);
+        atomicAdd(&acc->bnr, bn);
+        atomicMax(&acc->maxr, mx);
+        atomicMin(&acc->minr, mn);
+    } else {
+        atomicAdd(&acc->s2c, s2);
+        atomicAdd(&acc->bnc, bn);
+        atomicMax(&acc->maxc, mx);
+        atomicMin(&acc->minc, mn);
     }
 }
 
-// One wavefront per row: lanes stride over the row's entries and mark the
-// diagonal (col - row) each one lies on.
+inline unsigned stats_grid(int64_t n)
+{
+    int64_t g = ceil_div(n, (int64_t)kTB * 8);
+    return (unsigned)(g < 1 ? 1 : g > 512 ? 512 : g);
+}
+
+// Diagonal occupancy bitmap: bit (col - row + R - 1) is set for every entry.
+//
+// Small spans (the bitmap and a row_ptr slice fit in one workgroup's LDS):
+// workgroup p owns a contiguous range of rows, marks its entries' diagonals
+// in a private LDS bitmap (one thread per entry, its row found by binary
+// search in the LDS copy of the range's row_ptr slice), and writes the
+// bitmap out whole; k_diag_or then ORs the per-workgroup bitmaps word by
+// word.  No global atomics.
+//
+// Large spans: one wavefront per row marks the global bitmap with atomicOr,
+// skipping the atomic when the bit is already set (bits only ever get set,
+// and the main diagonal alone gets one hit per row).
+constexpr int64_t kDiagLdsRows = 2048;    // rows per workgroup (8 KiB row_ptr slice)
+constexpr int kDiagParts = 256;           // workgroups (partial bitmaps)
+
+__global__ __launch_bounds__(kTB) void k_diag_lds(const int32_t *__restrict__ rp,
+                                                  const int32_t *__restrict__ col, int64_t R,
+                                                  int64_t nw, int64_t rows_per,
+                                                  uint32_t *__restrict__ partial)
+{
+    extern __shared__ uint32_t sm[];
+    uint32_t *lbm = sm;
+    int32_t *lrp = reinterpret_cast<int32_t *>(sm + nw);
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per < R ? (int64_t)blockIdx.x * rows_per : R;
+    const int64_t r1 = r0 + rows_per < R ? r0 + rows_per : R;
+    const int nr = (int)(r1 - r0);
+    for (int64_t w = threadIdx.x; w < nw; w += kTB) lbm[w] = 0;
+    for (int i = threadIdx.x; i <= nr; i += kTB) lrp[i] = rp[r0 + i];
+    __syncthreads();
+    const int64_t k0 = lrp[0], k1 = lrp[nr];
+    constexpr int U = 4;  // column loads in flight per thread
+    for (int64_t kb = k0 + threadIdx.x; kb < k1; kb += U * kTB) {
+        int c[U];
+#pragma unroll
+        for (int u = 0; u < U; u++) c[u] = kb + u * kTB < k1 ? col[kb + u * kTB] : 0;
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int64_t k = kb + u * kTB;
+            if (k >= k1) break;
+            // last row i of the range with lrp[i] <= k (empty rows share their start)
+            int lo = 0, hi = nr - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (lrp[mid] <= k)
+                    lo = mid;
+                else
+                    hi = mid - 1;
+            }
+            const int64_t sidx = (int64_t)c[u] - (r0 + lo) + R - 1;
+            const uint32_t bit = 1u << (sidx & 31);
+            if (!(lbm[sidx >> 5] & bit)) atomicOr(&lbm[sidx >> 5], bit);
+        }
+    }
+    __syncthreads();
+    uint32_t *out = partial + (int64_t)blockIdx.x * nw;
+    for (int64_t w = threadIdx.x; w < nw; w += kTB) out[w] = lbm[w];
+}
+
+// Block of 1024 threads = 64 words x 16 slices of the partial bitmaps.
+__global__ __launch_bounds__(1024) void k_diag_or(const uint32_t *__restrict__ partial, int64_t P,
+                                                  int64_t nw, uint32_t *__restrict__ bm)
+{
+    __shared__ uint32_t red[16][64];
+    const int lane = threadIdx.x % 64, sl = threadIdx.x / 64;
+    const int64_t w = (int64_t)blockIdx.x * 64 + lane;
+    uint32_t v = 0;
+    if (w < nw)
+        for (int64_t p = sl; p < P; p += 16) v |= partial[p * nw + w];
+    red[sl][lane] = v;
+    __syncthreads();
+    if (sl == 0 && w < nw) {
+        for (int q = 1; q < 16; q++) v |= red[q][lane];
+        bm[w] = v;
+    }
+}
+
 __global__ __launch_bounds__(kTB) void k_mark_diags(const int32_t *__restrict__ rp,
                                                     const int32_t *__restrict__ col, int64_t R,
                                                     uint32_t *__restrict__ bm)
@@ -85,8 +186,6 @@ __global__ __launch_bounds__(kTB) void k_mark_diags(const int32_t *__restrict__ 
     for (int64_t i = ((int64_t)blockIdx.x * kTB + threadIdx.x) / kWave; i < R; i += waves) {
         for (int64_t k = rp[i] + lane; k < rp[i + 1]; k += kWave) {
             int64_t sidx = (int64_t)col[k] - i + R - 1;
-            // bits only ever get set: skip the atomic when the word already has it
-            // (the main diagonal alone gets one hit per row)
             const uint32_t bit = 1u << (sidx & 31);
             if (!(__hip_atomic_load(&bm[sidx >> 5], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit))
                 atomicOr(&bm[sidx >> 5], bit);
@@ -117,6 +216,32 @@ double population_dev(int64_t n, int64_t Z, uint64_t s2)
 
 }  // namespace
 
+void diag_bitmap(const int32_t *rp, const int32_t *col, int64_t R, int64_t C, int64_t Z,
+                 uint32_t *bm, hipStream_t s)
+{
+    const int64_t nw = (R > 0 && C > 0) ? ceil_div(R + C - 1, 32) : 0;
+    if (nw == 0) return;
+    const int64_t P = std::min<int64_t>(kDiagParts, R);
+    const int64_t rows_per = ceil_div(R, P);
+    if (Z > 0 && (nw + rows_per + 1) * 4 <= max_lds_bytes() && rows_per <= kDiagLdsRows &&
+        std::getenv("GS_DIAG_GLOBAL") == nullptr) {
+        DevBuf part;
+        part.alloc((size_t)(P * nw) * 4, s);
+        const size_t lds = (size_t)(nw + rows_per + 1) * 4;
+        k_diag_lds<<<(unsigned)P, kTB, lds, s>>>(rp, col, R, nw, rows_per, part.as<uint32_t>());
+        GS_HIP(hipGetLastError());
+        k_diag_or<<<(unsigned)ceil_div(nw, 64), 1024, 0, s>>>(part.as<uint32_t>(), P, nw, bm);
+        GS_HIP(hipGetLastError());
+        GS_HIP(hipStreamSynchronize(s));  // before part is freed
+        return;
+    }
+    GS_HIP(hipMemsetAsync(bm, 0, (size_t)nw * 4, s));
+    if (Z > 0) {
+        k_mark_diags<<<elem_grid(R * kWave), kTB, 0, s>>>(rp, col, R, bm);
+        GS_HIP(hipGetLastError());
+    }
+}
+
 void features_from_csr(const gs_matrix_ &csr, hipStream_t s, gs_features *out)
 {
     const int64_t R = csr.R, C = csr.C, Z = csr.Z;
@@ -131,7 +256,7 @@ void features_from_csr(const gs_matrix_ &csr, hipStream_t s, gs_features *out)
     GS_HIP(hipMemcpyAsync(acc.p, &h, sizeof h, hipMemcpyHostToDevice, s));
     GS_HIP(hipMemsetAsync(ndv.p, 0, sizeof(unsigned long long), s));
     if (R > 0) {
-        k_count_stats<<<elem_grid(R), kTB, 0, s>>>(rp, nullptr, R, 1, acc.as<FeatAcc>());
+        k_count_stats<<<stats_grid(R), kTB, 0, s>>>(rp, nullptr, R, 1, acc.as<FeatAcc>());
         GS_HIP(hipGetLastError());
     }
     if (C > 0) {
@@ -141,15 +266,13 @@ void features_from_csr(const gs_matrix_ &csr, hipStream_t s, gs_features *out)
             k_col_hist<<<elem_grid(Z), kTB, 0, s>>>(col, Z, cc.as<int32_t>());
             GS_HIP(hipGetLastError());
         }
-        k_count_stats<<<elem_grid(C), kTB, 0, s>>>(nullptr, cc.as<int32_t>(), C, 0, acc.as<FeatAcc>());
+        k_count_stats<<<stats_grid(C), kTB, 0, s>>>(nullptr, cc.as<int32_t>(), C, 0, acc.as<FeatAcc>());
         GS_HIP(hipGetLastError());
     }
     if (Z > 0) {
         const int64_t nw = ceil_div(R + C - 1, 32);
         bm.alloc((size_t)nw * 4, s);
-        GS_HIP(hipMemsetAsync(bm.p, 0, (size_t)nw * 4, s));
-        k_mark_diags<<<elem_grid(R * kWave), kTB, 0, s>>>(rp, col, R, bm.as<uint32_t>());
-        GS_HIP(hipGetLastError());
+        diag_bitmap(rp, col, R, C, Z, bm.as<uint32_t>(), s);
         k_popc_total<<<elem_grid(nw), kTB, 0, s>>>(bm.as<uint32_t>(), nw, ndv.as<unsigned long long>());
         GS_HIP(hipGetLastError());
     }

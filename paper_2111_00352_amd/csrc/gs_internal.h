@@ -119,13 +119,14 @@ struct gs_matrix_ {
     int64_t n_medium_rows = 0, n_medium_chunks = 0;  // long rows of at most csr_wg_thr entries
     int csr_wg_thr = 0;
     bool csr_sorted = false; // items ordered by decreasing length
+    bool csr_planned = false; // plan_csr has run (a CSR built only for its features has no plan)
     // COO: rows with no entries (zeroed by the COO kernel)
     int64_t n_empty_rows = 0;
     gs::DevBuf empty_rows;
     // COO: chunk boundaries (row-aligned unless a row is longer than a chunk)
-    // and the chunks where a split row starts
-    int64_t n_coo_chunks = 0, n_coo_starts = 0;
-    gs::DevBuf coo_bounds, coo_starts;
+    // and the rows split over several chunks, {row, first chunk, pieces, 0}
+    int64_t n_coo_chunks = 0, n_coo_split = 0;
+    gs::DevBuf coo_bounds, coo_split;
 
     // F-dependent workspace (partials / carries), grown on demand.
     gs::DevBuf work;
@@ -169,7 +170,9 @@ struct CanonCOO {
 void canonicalize(const gs_coo &A, bool assume_canonical, hipStream_t s, CanonCOO &out);
 
 // Builds a CSR handle from canonical COO (takes ownership of col/val).
-gs_matrix_ *csr_from_canon(CanonCOO &&c, hipStream_t s);
+// plan = false leaves the SpMM work plan to the first use of the handle
+// (feature extraction reads only row_ptr / col).
+gs_matrix_ *csr_from_canon(CanonCOO &&c, hipStream_t s, bool plan = true);
 
 // Builds format fmt from a CSR handle (not consumed).
 gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint64_t max_bytes,
@@ -191,6 +194,10 @@ int64_t count_blocks(const gs_matrix_ &csr, int b, hipStream_t s);
 // --------------------------------------------------- features (gs_features)
 
 void features_from_csr(const gs_matrix_ &csr, hipStream_t s, gs_features *out);
+// Diagonal occupancy bitmap of a CSR matrix: bit (col - row + R - 1) of
+// bm[ceil((R+C-1)/32)] set for every entry; bm need not be cleared.
+void diag_bitmap(const int32_t *rp, const int32_t *col, int64_t R, int64_t C, int64_t Z,
+                 uint32_t *bm, hipStream_t s);
 
 // ------------------------------------------------------- spmm (gs_spmm_*)
 
@@ -216,6 +223,8 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
 // Workgroups of 256 threads the device keeps resident at full occupancy
 // (compute units x 8), queried once.
 int resident_workgroups();
+// LDS bytes one workgroup may use (the device's limit), queried once.
+int64_t max_lds_bytes();
 
 // Vectorised ELL / DIA paths; false when F / alignment do not allow them.
 bool spmm_ell_fast(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,

@@ -80,6 +80,18 @@ int resident_workgroups()
     return n;
 }
 
+int64_t max_lds_bytes()
+{
+    static int64_t n = 0;
+    if (n == 0) {
+        int dev = 0, v = 0;
+        GS_HIP(hipGetDevice(&dev));
+        GS_HIP(hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev));
+        n = v > 0 ? v : 65536;
+    }
+    return n;
+}
+
 }  // namespace gs
 
 using namespace gs;

@@ -31,7 +31,7 @@
 #include "gs_internal.h"
 
 namespace gs {
-gs_matrix_ *build_csr(const gs_coo *A, const gs_build_opts &o, hipStream_t s);
+gs_matrix_ *build_csr(const gs_coo *A, const gs_build_opts &o, hipStream_t s, bool plan);
 void run_spmm(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
               hipStream_t s);
 void check_coo(const gs_coo *A);
@@ -220,7 +220,7 @@ Entry &lookup(gs_ctx_ &c, uint64_t key, const gs_coo *A, hipStream_t s)
     try {
         const double t0 = now_s();
         gs_build_opts o = {c.opts.bsr_block, 0, c.opts.max_bytes};
-        gs_matrix_ *csr = build_csr(A, o, s);
+        gs_matrix_ *csr = build_csr(A, o, s, false);  // planned when CSR is first run
         e->built[GS_CSR] = csr;
         features_from_csr(*csr, s, &e->feat);
         const int b = c.opts.bsr_block;
@@ -246,6 +246,10 @@ gs_matrix_ &ensure_built(gs_ctx_ &c, Entry &e, int fmt, hipStream_t s)
         const double t0 = now_s();
         e.built[fmt] = convert_from_csr(*e.built[GS_CSR], fmt, c.opts.bsr_block, c.opts.max_bytes, s,
                                         nullptr);
+        e.t_convert[fmt] = now_s() - t0;
+    } else if (fmt == GS_CSR && !e.built[fmt]->csr_planned) {
+        const double t0 = now_s();
+        plan_csr(*e.built[fmt], s);
         e.t_convert[fmt] = now_s() - t0;
     }
     return *e.built[fmt];

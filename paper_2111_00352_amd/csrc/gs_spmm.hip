@@ -155,13 +155,15 @@ __global__ __launch_bounds__(kBlock) void k_csr_combine(const int32_t *__restric
 
 // ---------------------------------------------------------------- COO
 // Segmented reduction over the (row, col)-sorted triplets.  Group q owns
-// entries [q*CH, (q+1)*CH).  Row boundaries inside the chunk are found with
-// a ballot over "row differs from the previous entry"; a segment is written
-// straight to Y unless its row continues into a neighbouring chunk, in which
-// case its partial goes to a carry slot: slot H (index 0) for the chunk's
-// first segment when that row began in an earlier chunk, slot T (index 1)
-// for the chunk's last segment when its row begins here and continues.
-// k_coo_fixup then adds each spanning row's carries in chunk order.
+// entries [bounds[q], bounds[q+1]): whole rows packed up to CH entries, or
+// one CH-entry piece of a row longer than CH.  Row boundaries inside the
+// chunk are found with a ballot over "row differs from the previous entry";
+// a segment is written straight to Y unless its row continues into a
+// neighbouring chunk (only a split row does), in which case its partial
+// goes to a carry slot: slot H (index 0) for the chunk's first segment when
+// that row began in an earlier chunk, slot T (index 1) for the chunk's last
+// segment when its row begins here and continues.  k_coo_fixup then adds
+// each split row's carries in chunk order.
 
 template <int VEC>
 __device__ __forceinline__ void coo_flush(const Acc<VEC> &acc, int64_t row, bool first_seg,
@@ -253,16 +255,13 @@ __global__ __launch_bounds__(kBlock) void k_coo_main(int64_t Z, const int32_t *_
                    active);
 }
 
-// Groups [0, n_starts): chunk starts[e], whose last segment begins a row
-// that runs on into later chunks, adds that row's carries (slot T of its
-// chunk, then slot H of the following chunks while the row continues) and
-// writes Y.  Groups after that zero the empty rows.
+// Groups [0, n_split): split row e (the int4 {row, first chunk q, piece
+// count n, 0}) adds its carries in chunk order, slot T of chunk q and then
+// slot H of chunks q+1 .. q+n-1, eight loads in flight, and writes Y.  The
+// groups after those zero the empty rows.
 template <int VEC, int G>
-__global__ __launch_bounds__(kBlock) void k_coo_fixup(int64_t Z, const int32_t *__restrict__ row,
-                                                      const int32_t *__restrict__ bounds,
-                                                      int64_t n_chunks,
-                                                      const int32_t *__restrict__ starts,
-                                                      int64_t n_starts, const float *__restrict__ work,
+__global__ __launch_bounds__(kBlock) void k_coo_fixup(const int4 *__restrict__ split, int64_t n_split,
+                                                      const float *__restrict__ work,
                                                       const int32_t *__restrict__ empty_rows,
                                                       int64_t n_empty, float *__restrict__ Y,
                                                       int64_t ldy, int64_t F)
@@ -272,25 +271,28 @@ __global__ __launch_bounds__(kBlock) void k_coo_fixup(int64_t Z, const int32_t *
     const int64_t c0 = (int64_t)blockIdx.y * (G * VEC) + (int64_t)lane * VEC;
     const int64_t e = (int64_t)blockIdx.x * GPB + g;
     if (c0 >= F) return;
-    if (e < n_starts) {
-        const int64_t q = starts[e];
-        const int32_t r = row[bounds[q + 1] - 1];
+    if (e < n_split) {
+        const int4 d = split[e];
+        const int64_t q = d.y, n = d.z;
         Acc<VEC> acc;
         acc.zero();
-        const Vec<VEC> t = ld_vec<VEC>(work + (q * 2 + 1) * F + c0);
+        for (int64_t p0 = 0; p0 < n; p0 += 8) {
+            Vec<VEC> h[8];
 #pragma unroll
-        for (int i = 0; i < VEC; i++) acc.v[i] = t.v[i];
-        for (int64_t p = q + 1; p < n_chunks; p++) {
-            const Vec<VEC> h = ld_vec<VEC>(work + (p * 2 + 0) * F + c0);
+            for (int u = 0; u < 8; u++) {
+                const int64_t p = p0 + u < n ? p0 + u : n - 1;
+                h[u] = ld_vec<VEC>(work + ((q + p) * 2 + (p == 0 ? 1 : 0)) * F + c0);
+            }
 #pragma unroll
-            for (int i = 0; i < VEC; i++) acc.v[i] += h.v[i];
-            const int64_t p1 = bounds[p + 1];
-            const bool whole = row[p1 - 1] == r && p1 < Z && row[p1] == r;
-            if (!whole) break;
+            for (int u = 0; u < 8; u++) {
+                if (p0 + u >= n) break;
+#pragma unroll
+                for (int i = 0; i < VEC; i++) acc.v[i] += h[u].v[i];
+            }
         }
-        st_vec_stream<VEC>(Y + (int64_t)r * ldy + c0, acc.vec());
+        st_vec_stream<VEC>(Y + (int64_t)d.x * ldy + c0, acc.vec());
     } else {
-        const int64_t k = e - n_starts;
+        const int64_t k = e - n_split;
         if (k >= n_empty) return;
         Vec<VEC> z;
 #pragma unroll
@@ -511,7 +513,8 @@ void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s)
     std::vector<int32_t> rp((size_t)m.R + 1);
     GS_HIP(hipMemcpyAsync(rp.data(), row_ptr, rp.size() * 4, hipMemcpyDeviceToHost, s));
     GS_HIP(hipStreamSynchronize(s));
-    std::vector<int32_t> empty, bounds{0}, starts;
+    std::vector<int32_t> empty, bounds{0};
+    std::vector<int4> split;
     int64_t cur = 0;
     for (int64_t i = 0; i < m.R; i++) {
         const int32_t pos = rp[i], len = rp[i + 1] - rp[i];
@@ -521,7 +524,7 @@ void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s)
         }
         if (len > chunk) {
             if (pos > bounds.back()) bounds.push_back(pos);
-            starts.push_back((int32_t)bounds.size() - 1);
+            split.push_back(make_int4((int)i, (int)bounds.size() - 1, (len + chunk - 1) / chunk, 0));
             for (int32_t o = chunk; o < len; o += chunk) bounds.push_back(pos + o);
             bounds.push_back(pos + len);
             cur = 0;
@@ -535,14 +538,14 @@ void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s)
     }
     if (m.Z > bounds.back()) bounds.push_back((int32_t)m.Z);
     m.n_coo_chunks = (int64_t)bounds.size() - 1;
-    m.n_coo_starts = (int64_t)starts.size();
+    m.n_coo_split = (int64_t)split.size();
     m.n_empty_rows = (int64_t)empty.size();
     m.coo_bounds.alloc(bounds.size() * 4, s);
-    m.coo_starts.alloc(starts.size() * 4, s);
+    m.coo_split.alloc(split.size() * sizeof(int4), s);
     m.empty_rows.alloc(empty.size() * 4, s);
     GS_HIP(hipMemcpyAsync(m.coo_bounds.p, bounds.data(), bounds.size() * 4, hipMemcpyHostToDevice, s));
-    if (!starts.empty())
-        GS_HIP(hipMemcpyAsync(m.coo_starts.p, starts.data(), starts.size() * 4, hipMemcpyHostToDevice, s));
+    if (!split.empty())
+        GS_HIP(hipMemcpyAsync(m.coo_split.p, split.data(), split.size() * sizeof(int4), hipMemcpyHostToDevice, s));
     if (!empty.empty())
         GS_HIP(hipMemcpyAsync(m.empty_rows.p, empty.data(), empty.size() * 4, hipMemcpyHostToDevice, s));
     GS_HIP(hipStreamSynchronize(s));
@@ -553,6 +556,7 @@ void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s)
 void spmm_csr(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
               hipStream_t s)
 {
+    if (!m.csr_planned) plan_csr(m, s);
     if (spmm_csr_vec4(m, X, ldx, Y, ldy, F, s)) return;
     const Shape sh = pick_shape(X, ldx, Y, ldy, F);
     if (m.n_long_chunks) ensure_work(m, (size_t)m.n_long_chunks * F * 4, s);
@@ -580,7 +584,7 @@ void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
 {
     const Shape sh = pick_shape(X, ldx, Y, ldy, F);
     const int64_t n_chunks = m.n_coo_chunks;
-    if (m.n_coo_starts) ensure_work(m, (size_t)n_chunks * 2 * F * 4, s);
+    if (m.n_coo_split) ensure_work(m, (size_t)n_chunks * 2 * F * 4, s);
     dispatch(sh, [&]<int VEC, int G>() {
         constexpr int GPB = kBlock / G;
         if (n_chunks) {
@@ -591,11 +595,10 @@ void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
                                                        m.work.as<float>());
             GS_HIP(hipGetLastError());
         }
-        const int64_t groups = m.n_coo_starts + m.n_empty_rows;
+        const int64_t groups = m.n_coo_split + m.n_empty_rows;
         if (groups) {
             dim3 g2(u32_grid(ceil_div(groups, GPB)), (unsigned)sh.fslices);
-            k_coo_fixup<VEC, G><<<g2, kBlock, 0, s>>>(m.Z, m.row.as<int32_t>(), m.coo_bounds.as<int32_t>(),
-                                                      n_chunks, m.coo_starts.as<int32_t>(), m.n_coo_starts,
+            k_coo_fixup<VEC, G><<<g2, kBlock, 0, s>>>(m.coo_split.as<int4>(), m.n_coo_split,
                                                       m.work.as<float>(), m.empty_rows.as<int32_t>(),
                                                       m.n_empty_rows, Y, ldy, F);
             GS_HIP(hipGetLastError());

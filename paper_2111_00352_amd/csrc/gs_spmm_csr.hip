@@ -278,6 +278,7 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
         GS_HIP(hipMemcpyAsync(m.long_rows.p, lrows.data(), lrows.size() * 4, hipMemcpyHostToDevice, s));
     GS_HIP(hipMemcpyAsync(m.long_first.p, lfirst.data(), lfirst.size() * 4, hipMemcpyHostToDevice, s));
     GS_HIP(hipStreamSynchronize(s));
+    m.csr_planned = true;
 }
 
 // ------------------------------------------------------------- launcher

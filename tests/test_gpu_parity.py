@@ -189,6 +189,28 @@ def test_long_and_dense_rows(fmt):
     check_spmm(case, m, X)
 
 
+@pytest.mark.parametrize("chunk", ["128", "16"])
+def test_coo_row_aligned_chunks(monkeypatch, chunk):
+    # rows at and around the chunk length, split rows back to back, at the
+    # first and last row, with empty rows between them
+    monkeypatch.setenv("GS_COO_CHUNK", chunk)
+    lens = [300, 0, 127, 128, 129, 0, 256, 257, 1000, 1, 0, 0, 5, 128, 16, 17, 15, 640, 0, 3, 129]
+    C = 2000
+    rng = np.random.default_rng(77)
+    rows, cols = [], []
+    for i, n in enumerate(lens):
+        rows.append(np.full(n, i, np.int32))
+        cols.append(np.sort(rng.choice(C, n, replace=False)).astype(np.int32))
+    row, col = np.concatenate(rows), np.concatenate(cols)
+    val = rng.uniform(-1, 1, row.size).astype(np.float32)
+    val[val == 0] = 0.5
+    row, col, val = graphgen.shuffled(row, col, val, 78)
+    case = Case(len(lens), C, row, col, val)
+    for F in (4, 64, 132):
+        X = graphgen.features_x(C, F, 79 + F, "normal")
+        check_spmm(case, case.build("coo"), X)
+
+
 def test_empty_and_degenerate_matrices():
     for R, C in ((0, 0), (0, 5), (5, 0), (7, 9)):
         case = Case(R, C, np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
@@ -365,6 +387,18 @@ def test_trained_model_choice_is_near_the_profiled_best():
         chosen = gs.SelectContext("model").select(1, case.d_row, case.d_col, case.d_val, shape, g.F)
         ratios.append(min(times.values()) / times[chosen])
     assert np.exp(np.mean(np.log(ratios))) > 0.6, ratios
+
+
+@pytest.mark.parametrize("path", ["lds", "global"])
+def test_diagonal_bitmap_paths_agree(monkeypatch, path):
+    # the per-workgroup LDS bitmap and the global-atomic bitmap must give the
+    # same diagonal set (features N_diags and the DIA layout)
+    if path == "global":
+        monkeypatch.setenv("GS_DIAG_GLOBAL", "1")
+    for case in (_random_case(3001, 2500, 20000, 91), _random_case(300, 7000, 9000, 92, empty=0.3),
+                 _case_from_graph(graphgen.scaled(3), shuffle_seed=93)):
+        check_features(case)
+        check_layout(case, "dia")
 
 
 @pytest.mark.parametrize("merge", ["0", "1"])
