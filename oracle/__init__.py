@@ -12,6 +12,7 @@ names the passage of the paper (arXiv 2111.00352) it follows:
 * storage formats COO/CSR/DIA/BSR ............ Sec. 2.2 (ELL: padded row packing)
 * SpMM Y = A.X ................................ Sec. 2.1
 * features F1..F19 ............................ Sec. 4.4, Table 2
+* two-layer GCN forward / backward (gcn.py) ... Sec. 2.1, Sec. 5.1 (numpy fp64)
 
 ``check_spmm`` applies the acceptance bound |Y - Y_ref| <= 1e-5 * (|A|.|X|) + 1e-6
 elementwise, evaluated in fp64.
@@ -76,6 +77,7 @@ def lib():
             "or_features": (ctypes.c_int, [i64, i64, i64, p, p, p, p]),
             "or_spmm": (ctypes.c_int, [i64, p, p, p, p, i64, i64, p, p]),
             "or_spmm_rows": (ctypes.c_int, [i64, p, p, p, p, p, i64, i64, p, p]),
+            "or_spmm64": (ctypes.c_int, [i64, p, p, p, p, i64, i64, p]),
             "or_num_threads": (ctypes.c_int, []),
         }
         for name, (res, args) in sig.items():
@@ -208,6 +210,16 @@ def spmm(R, row_ptr, col, val, X):
     M = np.empty((R, F), np.float64)
     lib().or_spmm(R, _p(row_ptr), _p(col), _p(val), _p(X), F, F, _p(Y), _p(M))
     return Y, M
+
+
+def spmm64(R, row_ptr, col, val, X):
+    """SpMM (Sec. 2.1) of an fp64 dense operand, summed in fp64: Y64[R, F]."""
+    row_ptr, col, val = _i32(row_ptr), _i32(col), _f32(val)
+    X = np.ascontiguousarray(X, dtype=np.float64)
+    F = X.shape[1]
+    Y = np.empty((R, F), np.float64)
+    lib().or_spmm64(R, _p(row_ptr), _p(col), _p(val), _p(X), F, F, _p(Y))
+    return Y
 
 
 def spmm_rows(rows, row_ptr, col, val, X):

@@ -408,6 +408,25 @@ int or_spmm(int64_t R, const int32_t *row_ptr, const int32_t *col, const float *
     return OR_OK;
 }
 
+/* The same sum with an fp64 dense operand (Sec. 2.1): used where the dense
+ * input is itself an exact fp64 intermediate (a GNN layer's hidden features
+ * or gradients), so that nothing is rounded to fp32 along a layer chain. */
+int or_spmm64(int64_t R, const int32_t *row_ptr, const int32_t *col, const float *val,
+              const double *X, int64_t ldx, int64_t F, double *Y)
+{
+    int64_t i;
+#pragma omp parallel for schedule(dynamic, 64)
+    for (i = 0; i < R; i++) {
+        for (int64_t f = 0; f < F; f++) {
+            double s = 0.0;
+            for (int64_t k = row_ptr[i]; k < row_ptr[i + 1]; k++)
+                s += (double)val[k] * X[(int64_t)col[k] * ldx + f];
+            Y[i * F + f] = s;
+        }
+    }
+    return OR_OK;
+}
+
 /* Same definition, for a chosen list of rows only (used to check sampled
  * outputs of very large problems one row at a time). */
 int or_spmm_rows(int64_t nsel, const int64_t *rows, const int32_t *row_ptr, const int32_t *col,

@@ -2,19 +2,20 @@
 
 Usage: python -m paper_2111_00352_amd.selector.compare [DATA.csv] [--folds 5] [--md OUT.md]
 
-The paper sets its gradient-boosted trees against other learned selectors
-(Sec. 6.4, Table 3: decision tree, k-nearest neighbour, support vector
-machine, multi-layer perceptron and a CNN; Fig. 11 their accuracy and
-inference time).  Every candidate here sees the same inputs (Table 2
-features plus the 16x16 block fill and F, min-max scaled with the training
-fold's range and clipped) and the same labels (Eq. 1 with w = 1, 1% ties)
-as ``train``, and is scored with the same grouped k-fold split (no matrix in
-both the training and the test fold) on:
+The paper sets its gradient-boosted trees against a decision tree and a CNN
+from prior format-selection work (Sec. 5.2, Sec. 6.2 and its table of
+inference time, accuracy and realised speedup) and against an MLP, 1-nearest
+neighbour and an SVM (Sec. 6.4, accuracy and prediction time).  Every
+candidate here sees the same inputs (Table 2 features plus the 16x16 block
+fill and F, min-max scaled with the training fold's range and clipped) and
+the same labels (Eq. 1 with w = 1, 1% ties) as ``train``, and is scored with
+the same grouped k-fold split (no matrix in both the training and the test
+fold) on:
   * accuracy against the profiled label;
   * geometric-mean speedup of the chosen format over fixed CSR, and the
     fraction of the profiling oracle's performance (Sec. 6.3);
   * the time of one prediction (one feature vector, the selector's use),
-    median over repeated single-sample calls.
+    median over repeated single-sample calls of the scikit-learn model.
 The CNN (which reads the matrix as an image) is not included: its input is
 not the feature vector the library extracts.
 """
