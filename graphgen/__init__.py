@@ -164,7 +164,7 @@ def _tiny(seed_g, seed_x, n=2048, F=64):
     row, col = _sym_with_self(u, v, n)
     val = _gcn_values(row, col, n)
     X = _um11(_rng(seed_x), (n, F))
-    return row, col, val, X, dict(n=n, F=F, p=4.0 / (n - 1))
+    return row, col, val, X, dict(n=n, F=F, p=4.0 / (n - 1), symmetric=True)
 
 
 def _powerlaw(seed_g, seed_x, n=100_000, F=128, gamma=2.1, mean_deg=10.0, cap=5000):
@@ -173,7 +173,7 @@ def _powerlaw(seed_g, seed_x, n=100_000, F=128, gamma=2.1, mean_deg=10.0, cap=50
     row, col = _sym_with_self(u, v, n)
     val = _gcn_values(row, col, n)
     X = _normal(_rng(seed_x), (n, F))
-    return row, col, val, X, dict(n=n, F=F, gamma=gamma, mean_deg=mean_deg, cap=cap)
+    return row, col, val, X, dict(n=n, F=F, gamma=gamma, mean_deg=mean_deg, cap=cap, symmetric=True)
 
 
 def _mesh(seed_g, seed_x, m=512, F=64):
@@ -187,7 +187,7 @@ def _mesh(seed_g, seed_x, m=512, F=64):
     row, col = _canon_from_keys(np.concatenate(parts), n)
     val = _u01_closed_top(_rng(seed_g), row.size)
     X = _um11(_rng(seed_x), (n, F))
-    return row, col, val, X, dict(n=n, m=m, F=F)
+    return row, col, val, X, dict(n=n, m=m, F=F, symmetric=False)
 
 
 def _blocks(seed_g, seed_x, n_comm=12_800, size=16, F=256, p=0.8, inter=2):
@@ -207,7 +207,7 @@ def _blocks(seed_g, seed_x, n_comm=12_800, size=16, F=256, p=0.8, inter=2):
     row, col = _sym_with_self(u, v, n)
     val = _gcn_values(row, col, n)
     X = _normal(_rng(seed_x), (n, F))
-    return row, col, val, X, dict(n=n, n_comm=n_comm, size=size, F=F, p=p, inter=inter)
+    return row, col, val, X, dict(n=n, n_comm=n_comm, size=size, F=F, p=p, inter=inter, symmetric=True)
 
 
 def _large(seed_g, seed_x, n=2_000_000, F=128, gamma=2.0, mean_deg=25.0, cap=None):
@@ -220,7 +220,7 @@ def _large(seed_g, seed_x, n=2_000_000, F=128, gamma=2.0, mean_deg=25.0, cap=Non
     rs = np.bincount(row, weights=raw, minlength=n)
     val = (raw / rs[row]).astype(np.float32)
     X = _normal(_rng(seed_x), (n, F))
-    return row, col, val, X, dict(n=n, F=F, gamma=gamma, mean_deg=mean_deg, cap=cap)
+    return row, col, val, X, dict(n=n, F=F, gamma=gamma, mean_deg=mean_deg, cap=cap, symmetric=False)
 
 
 _BUILDERS = {1: _tiny, 2: _powerlaw, 3: _mesh, 4: _blocks, 5: _large}

@@ -94,11 +94,12 @@ def magnitudes(g: Graph, X, W1, W2, T):
                 dZ1=dZ1, dW1=dW1)
 
 
-def relu_ambiguity(g: Graph, X, ref, mag, eps):
+def relu_ambiguity(g: Graph, X, ref, mag, eps, atol=0.0):
     """Extra bound on dW1 from ReLU decisions an fp32 evaluation may take the
-    other way: entries of P1 within eps * |P1| of zero.  Flipping one such
-    decision (i, h) changes dW1[:, h] by at most |dH1[i, h]| (|X|^T |A|^T e_i)."""
-    amb = np.abs(ref["P1"]) <= eps * mag["P1"]
+    other way: entries of P1 within eps * |P1| + atol of zero (the error bound
+    of the fp32 P1).  Flipping one such decision (i, h) changes dW1[:, h] by at
+    most |dH1[i, h]| (|X|^T |A|^T e_i)."""
+    amb = np.abs(ref["P1"]) <= eps * mag["P1"] + atol
     E = np.abs(mag["dH1"]) * amb
     extra = np.abs(np.asarray(X, dtype=np.float64)).T @ g.agg_t(E, absolute=True)
     return extra, int(amb.sum())
