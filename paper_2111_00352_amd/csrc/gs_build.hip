@@ -157,12 +157,6 @@ __global__ __launch_bounds__(kTB) void k_unpack_sorted(const uint64_t *__restric
     if (lane_id() == 0 && f) atomicOr(flags, f);
 }
 
-int bits_for(int64_t maxval)
-{
-    int b = 0;
-    while (b < 63 && (1ll << b) <= maxval) b++;
-    return b;
-}
 
 // ------------------------------------------------------------------- CSR
 
@@ -538,6 +532,41 @@ inline unsigned elem_grid(int64_t n)
 
 // ======================================================================
 
+int bits_for(int64_t maxval)
+{
+    int b = 0;
+    while (b < 63 && (1ll << b) <= maxval) b++;
+    return b;
+}
+
+void radix_sort_pairs(uint64_t *ka, uint64_t *kb, uint32_t *pa, uint32_t *pb, int64_t n,
+                      const std::vector<int> &shifts, hipStream_t s, uint64_t **keys,
+                      uint32_t **perm)
+{
+    uint64_t *kin = ka, *kout = kb;
+    uint32_t *pin = nullptr, *pout = pa, *pspare = pb;
+    if (n > 0 && !shifts.empty()) {
+        const int64_t ntiles = ceil_div(n, kRT);
+        DevBuf hist;
+        hist.alloc((size_t)(256 * ntiles + 1) * 4, s);
+        for (size_t i = 0; i < shifts.size(); i++) {
+            k_radix_hist<<<(unsigned)ntiles, kTB, 0, s>>>(kin, n, shifts[i], ntiles, hist.as<int32_t>());
+            GS_LAUNCH_CHECK();
+            exclusive_scan_i32(hist.as<int32_t>(), hist.as<int32_t>(), 256 * ntiles, false, s);
+            k_radix_scatter<<<(unsigned)ntiles, kTB, 0, s>>>(kin, pin, n, shifts[i], ntiles,
+                                                             hist.as<int32_t>(), kout, pout);
+            GS_LAUNCH_CHECK();
+            std::swap(kin, kout);
+            uint32_t *used = pout;
+            pout = (pin == nullptr) ? pspare : pin;
+            pin = used;
+        }
+        GS_HIP(hipStreamSynchronize(s));  // before hist is freed
+    }
+    *keys = kin;
+    *perm = pin;
+}
+
 void canonicalize(const gs_coo &A, bool assume_canonical, hipStream_t s, CanonCOO &out)
 {
     const int64_t R = A.n_rows, C = A.n_cols, Z = A.nnz;
@@ -571,30 +600,17 @@ void canonicalize(const gs_coo &A, bool assume_canonical, hipStream_t s, CanonCO
     std::vector<int> shifts;
     for (int sft = 0; sft < bc; sft += 8) shifts.push_back(sft);
     for (int sft = 0; sft < br; sft += 8) shifts.push_back(32 + sft);
-    const int64_t ntiles = ceil_div(Z, kRT);
-    DevBuf k0, k1, p0, p1, hist;
+    DevBuf k0, k1, p0, p1;
     k0.alloc((size_t)Z * 8, s);
     k1.alloc((size_t)Z * 8, s);
     p0.alloc((size_t)Z * 4, s);
     p1.alloc((size_t)Z * 4, s);
-    hist.alloc((size_t)(256 * ntiles + 1) * 4, s);
     k_make_keys<<<elem_grid(Z), kTB, 0, s>>>(A.row, A.col, Z, k0.as<uint64_t>());
     GS_LAUNCH_CHECK();
-    uint64_t *kin = k0.as<uint64_t>(), *kout = k1.as<uint64_t>();
-    uint32_t *pin = nullptr, *pout = p0.as<uint32_t>();
-    uint32_t *pspare = p1.as<uint32_t>();
-    for (size_t i = 0; i < shifts.size(); i++) {
-        k_radix_hist<<<(unsigned)ntiles, kTB, 0, s>>>(kin, Z, shifts[i], ntiles, hist.as<int32_t>());
-        GS_LAUNCH_CHECK();
-        exclusive_scan_i32(hist.as<int32_t>(), hist.as<int32_t>(), 256 * ntiles, false, s);
-        k_radix_scatter<<<(unsigned)ntiles, kTB, 0, s>>>(kin, pin, Z, shifts[i], ntiles,
-                                                         hist.as<int32_t>(), kout, pout);
-        GS_LAUNCH_CHECK();
-        std::swap(kin, kout);
-        uint32_t *used = pout;
-        pout = (pin == nullptr) ? pspare : pin;
-        pin = used;
-    }
+    uint64_t *kin = nullptr;
+    uint32_t *pin = nullptr;
+    radix_sort_pairs(k0.as<uint64_t>(), k1.as<uint64_t>(), p0.as<uint32_t>(), p1.as<uint32_t>(), Z,
+                     shifts, s, &kin, &pin);
     GS_HIP(hipMemsetAsync(flags.p, 0, sizeof(int), s));
     k_unpack_sorted<<<elem_grid(Z), kTB, 0, s>>>(kin, pin, A.val, Z, out.row.as<int32_t>(),
                                                  out.col.as<int32_t>(), out.val.as<float>(),

@@ -159,6 +159,16 @@ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 void exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, bool out_has_total,
                         hipStream_t s);
 
+// Stable LSD radix sort of n 64-bit keys on the 8-bit digits at `shifts`,
+// least significant first, carrying a 32-bit payload that starts as the
+// identity (the key's input position).  Ping-pongs between (ka, pa) and
+// (kb, pb); *keys / *perm receive the buffers holding the result (*perm is
+// null when no pass ran: the identity).  Synchronises s.
+void radix_sort_pairs(uint64_t *ka, uint64_t *kb, uint32_t *pa, uint32_t *pb, int64_t n,
+                      const std::vector<int> &shifts, hipStream_t s, uint64_t **keys,
+                      uint32_t **perm);
+int bits_for(int64_t maxval);
+
 // ------------------------------------------------------ build (gs_build)
 
 struct CanonCOO {

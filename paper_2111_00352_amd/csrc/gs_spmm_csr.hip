@@ -194,90 +194,202 @@ int env_int(const char *name, int dflt)
 // The generic path runs every chunk item and combines every long row; the
 // vectorised path runs medium rows a workgroup each and only the huge rows'
 // chunks (combined by a second small launch).
+//
+// The plan is built on the device: every row gets the 64-bit key
+// (group << 32 | rank) with group 0 = medium, 1 = huge, 2 = short and rank =
+// maxlen - len for long rows, thr - len for short rows of a skewed matrix
+// (0 otherwise); a stable radix sort on those keys gives the row order
+// (natural order within equal keys), a scan of the rows' item counts gives
+// each row's first item, and one kernel writes the items.  A long row's
+// chunk slots are its item positions.
+
+namespace {
+
+struct PlanStats {
+    unsigned long long sum, sum2;
+    int maxlen, n_long, n_huge;
+};
+
+__global__ __launch_bounds__(kBlock) void k_plan_stats(const int32_t *__restrict__ rp, int64_t R,
+                                                       int thr, int wg_thr,
+                                                       PlanStats *__restrict__ st)
+{
+    constexpr int NW = kBlock / kWave;
+    __shared__ unsigned long long s_sum[NW], s_sum2[NW];
+    __shared__ int s_max[NW], s_long[NW], s_huge[NW];
+    unsigned long long sum = 0, sum2 = 0;
+    int mx = 0, nl = 0, nh = 0;
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < R;
+         i += (int64_t)gridDim.x * kBlock) {
+        const int len = rp[i + 1] - rp[i];
+        sum += (unsigned long long)len;
+        sum2 += (unsigned long long)len * (unsigned long long)len;
+        mx = len > mx ? len : mx;
+        nl += len > thr;
+        nh += len > wg_thr;
+    }
+    sum = wave_sum_u64(sum);
+    sum2 = wave_sum_u64(sum2);
+    mx = wave_max_i32(mx);
+    nl = wave_sum_i32(nl);
+    nh = wave_sum_i32(nh);
+    const int w = threadIdx.x / kWave;
+    if (threadIdx.x % kWave == 0) {
+        s_sum[w] = sum;
+        s_sum2[w] = sum2;
+        s_max[w] = mx;
+        s_long[w] = nl;
+        s_huge[w] = nh;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    for (int v = 1; v < NW; v++) {
+        sum += s_sum[v];
+        sum2 += s_sum2[v];
+        mx = s_max[v] > mx ? s_max[v] : mx;
+        nl += s_long[v];
+        nh += s_huge[v];
+    }
+    atomicAdd(&st->sum, sum);
+    atomicAdd(&st->sum2, sum2);
+    atomicMax(&st->maxlen, mx);
+    atomicAdd(&st->n_long, nl);
+    atomicAdd(&st->n_huge, nh);
+}
+
+__global__ __launch_bounds__(kBlock) void k_plan_keys(const int32_t *__restrict__ rp, int64_t R,
+                                                      int thr, int wg_thr, int sorted, int maxlen,
+                                                      uint64_t *__restrict__ keys)
+{
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < R;
+         i += (int64_t)gridDim.x * kBlock) {
+        const int len = rp[i + 1] - rp[i];
+        const uint64_t group = len > thr ? (len > wg_thr ? 1u : 0u) : 2u;
+        const uint32_t rank = group < 2 ? (uint32_t)(maxlen - len) : sorted ? (uint32_t)(thr - len) : 0u;
+        keys[i] = (group << 32) | rank;
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_plan_count(const int32_t *__restrict__ rp,
+                                                       const uint64_t *__restrict__ keys,
+                                                       const uint32_t *__restrict__ perm, int64_t R,
+                                                       int chunk, int32_t *__restrict__ cnt)
+{
+    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < R;
+         p += (int64_t)gridDim.x * kBlock) {
+        const int64_t r = perm ? perm[p] : p;
+        const int len = rp[r + 1] - rp[r];
+        cnt[p] = (keys[p] >> 32) < 2 ? (len + chunk - 1) / chunk : 1;
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_plan_items(const int32_t *__restrict__ rp,
+                                                       const uint32_t *__restrict__ perm,
+                                                       const int32_t *__restrict__ off, int64_t R,
+                                                       int chunk, int64_t n_long,
+                                                       int4 *__restrict__ items,
+                                                       int32_t *__restrict__ long_rows,
+                                                       int32_t *__restrict__ long_first)
+{
+    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < R;
+         p += (int64_t)gridDim.x * kBlock) {
+        const int r = perm ? (int)perm[p] : (int)p;
+        const int start = rp[r], len = rp[r + 1] - start, o = off[p];
+        if (p < n_long) {
+            long_rows[p] = r;
+            long_first[p] = o;
+            for (int j = 0, c = 0; c < len; j++, c += chunk)
+                items[o + j] = make_int4(r, start + c, len - c < chunk ? len - c : chunk, o + j);
+        } else {
+            items[o] = make_int4(r, start, len, -1);
+        }
+        if (p == 0) long_first[n_long] = off[n_long];
+    }
+}
+
+inline unsigned plan_grid(int64_t n)
+{
+    int64_t g = ceil_div(n, (int64_t)kBlock);
+    return (unsigned)(g < 1 ? 1 : g > 4096 ? 4096 : g);
+}
+
+}  // namespace
 
 void plan_csr(gs_matrix_ &m, hipStream_t s)
 {
     const int thr = env_int("GS_CSR_LONG_ROW", kCsrLongRow);
     const int chunk = std::min(env_int("GS_CSR_CHUNK", kCsrChunk), thr);
+    const int wg_thr = env_int("GS_CSR_WG_ROW", kCsrWgRow);
     m.csr_long_thr = thr;
     m.csr_chunk = chunk;
-    std::vector<int32_t> rp((size_t)m.R + 1);
-    GS_HIP(hipMemcpyAsync(rp.data(), m.row_ptr.p, rp.size() * 4, hipMemcpyDeviceToHost, s));
-    GS_HIP(hipStreamSynchronize(s));
+    m.csr_wg_thr = wg_thr;
+    const int64_t R = m.R;
+    const int32_t *rp = m.row_ptr.as<int32_t>();
 
-    // Skewed row lengths (coefficient of variation above 1/2): order by length.
-    double sum = 0, sum2 = 0;
-    for (int64_t i = 0; i < m.R; i++) {
-        const double l = rp[i + 1] - rp[i];
-        sum += l;
-        sum2 += l * l;
+    PlanStats st = {0, 0, 0, 0, 0};
+    if (R > 0) {
+        DevBuf d_st;
+        d_st.alloc(sizeof st, s);
+        GS_HIP(hipMemcpyAsync(d_st.p, &st, sizeof st, hipMemcpyHostToDevice, s));
+        k_plan_stats<<<plan_grid(R), kBlock, 0, s>>>(rp, R, thr, wg_thr, d_st.as<PlanStats>());
+        GS_HIP(hipGetLastError());
+        GS_HIP(hipMemcpyAsync(&st, d_st.p, sizeof st, hipMemcpyDeviceToHost, s));
+        GS_HIP(hipStreamSynchronize(s));
     }
-    const double mean = m.R ? sum / m.R : 0.0;
-    const double var = m.R ? std::max(0.0, sum2 / m.R - mean * mean) : 0.0;
+    // Skewed row lengths (coefficient of variation above 1/2): order by length.
+    const double mean = R ? (double)st.sum / (double)R : 0.0;
+    const double var = R ? std::max(0.0, (double)st.sum2 / (double)R - mean * mean) : 0.0;
     const int force = env_int("GS_CSR_SORT", 0);  // 1: never, 2: always
     bool sorted = mean > 0 && std::sqrt(var) > 0.5 * mean;
     if (force == 1) sorted = false;
     if (force == 2) sorted = true;
     m.csr_sorted = sorted;
+    const int64_t n_long = st.n_long, n_huge = st.n_huge;
+    m.n_long_rows = n_long;
+    m.n_medium_rows = n_long - n_huge;
+    m.n_short = R - n_long;
 
-    std::vector<int32_t> lrows;
-    std::vector<int4> shorts;
-    shorts.reserve((size_t)m.R);
-    for (int64_t i = 0; i < m.R; i++) {
-        const int32_t a = rp[i], len = rp[i + 1] - rp[i];
-        if (len > thr)
-            lrows.push_back((int32_t)i);
-        else
-            shorts.push_back(make_int4((int)i, a, len, -1));
+    int32_t h_off[3] = {0, 0, 0};
+    DevBuf ka, kb, pa, pb, cnt;
+    uint32_t *perm = nullptr;
+    if (R > 0) {
+        ka.alloc((size_t)R * 8, s);
+        kb.alloc((size_t)R * 8, s);
+        pa.alloc((size_t)R * 4, s);
+        pb.alloc((size_t)R * 4, s);
+        k_plan_keys<<<plan_grid(R), kBlock, 0, s>>>(rp, R, thr, wg_thr, sorted ? 1 : 0, st.maxlen,
+                                                    ka.as<uint64_t>());
+        GS_HIP(hipGetLastError());
+        std::vector<int> shifts;
+        for (int sft = 0; sft < bits_for(std::max(st.maxlen, thr)); sft += 8) shifts.push_back(sft);
+        shifts.push_back(32);
+        uint64_t *keys = nullptr;
+        radix_sort_pairs(ka.as<uint64_t>(), kb.as<uint64_t>(), pa.as<uint32_t>(), pb.as<uint32_t>(), R,
+                         shifts, s, &keys, &perm);
+        cnt.alloc((size_t)(R + 1) * 4, s);
+        k_plan_count<<<plan_grid(R), kBlock, 0, s>>>(rp, keys, perm, R, chunk, cnt.as<int32_t>());
+        GS_HIP(hipGetLastError());
+        exclusive_scan_i32(cnt.as<int32_t>(), cnt.as<int32_t>(), R, true, s);
+        const int64_t at[3] = {m.n_medium_rows, n_long, R};
+        for (int i = 0; i < 3; i++)
+            GS_HIP(hipMemcpyAsync(&h_off[i], cnt.as<int32_t>() + at[i], 4, hipMemcpyDeviceToHost, s));
+        GS_HIP(hipStreamSynchronize(s));
     }
-    // medium long rows (one workgroup each on the vectorised path) first,
-    // then huge ones (split across workgroups there); each in decreasing length
-    const int wg_thr = env_int("GS_CSR_WG_ROW", kCsrWgRow);
-    m.csr_wg_thr = wg_thr;
-    std::stable_sort(lrows.begin(), lrows.end(), [&](int32_t p, int32_t q) {
-        const int32_t lp = rp[p + 1] - rp[p], lq = rp[q + 1] - rp[q];
-        const bool hp = lp > wg_thr, hq = lq > wg_thr;
-        if (hp != hq) return hq;  // medium before huge
-        return lp > lq;
-    });
-    m.n_medium_rows = 0;
-    for (int32_t r : lrows) m.n_medium_rows += (rp[r + 1] - rp[r]) <= wg_thr;
-    if (sorted) {  // stable counting sort by decreasing length (short rows have <= thr entries)
-        std::vector<int64_t> start((size_t)thr + 2, 0);
-        for (const int4 &it : shorts) start[(size_t)(thr - it.z) + 1]++;
-        for (size_t i = 1; i < start.size(); i++) start[i] += start[i - 1];
-        std::vector<int4> by_len(shorts.size());
-        for (const int4 &it : shorts) by_len[(size_t)start[(size_t)(thr - it.z)]++] = it;
-        shorts.swap(by_len);
+    m.n_medium_chunks = h_off[0];
+    m.n_long_chunks = h_off[1];
+    m.n_items = h_off[2];
+    m.csr_items.alloc((size_t)m.n_items * sizeof(int4), s);
+    m.long_rows.alloc((size_t)n_long * 4, s);
+    m.long_first.alloc((size_t)(n_long + 1) * 4, s);
+    if (R > 0) {
+        k_plan_items<<<plan_grid(R), kBlock, 0, s>>>(rp, perm, cnt.as<int32_t>(), R, chunk, n_long,
+                                                     m.csr_items.as<int4>(), m.long_rows.as<int32_t>(),
+                                                     m.long_first.as<int32_t>());
+        GS_HIP(hipGetLastError());
+    } else {
+        GS_HIP(hipMemsetAsync(m.long_first.p, 0, 4, s));
     }
-    std::vector<int4> items;
-    std::vector<int32_t> lfirst;
-    int32_t slot = 0;
-    for (size_t k = 0; k < lrows.size(); k++) {
-        const int32_t r = lrows[k];
-        if ((int64_t)k == m.n_medium_rows) m.n_medium_chunks = slot;
-        lfirst.push_back(slot);
-        const int32_t a = rp[r], len = rp[r + 1] - rp[r];
-        for (int32_t o = 0; o < len; o += chunk) items.push_back(make_int4(r, a + o, std::min(chunk, len - o), slot++));
-    }
-    if ((int64_t)lrows.size() == m.n_medium_rows) m.n_medium_chunks = slot;
-    lfirst.push_back(slot);
-    m.n_short = (int64_t)shorts.size();
-    items.insert(items.end(), shorts.begin(), shorts.end());
-
-    m.n_items = (int64_t)items.size();
-    m.n_long_rows = (int64_t)lrows.size();
-    m.n_long_chunks = slot;
-    m.csr_items.alloc(items.size() * sizeof(int4), s);
-    m.long_rows.alloc(lrows.size() * 4, s);
-    m.long_first.alloc(lfirst.size() * 4, s);
-    if (!items.empty())
-        GS_HIP(hipMemcpyAsync(m.csr_items.p, items.data(), items.size() * sizeof(int4),
-                              hipMemcpyHostToDevice, s));
-    if (!lrows.empty())
-        GS_HIP(hipMemcpyAsync(m.long_rows.p, lrows.data(), lrows.size() * 4, hipMemcpyHostToDevice, s));
-    GS_HIP(hipMemcpyAsync(m.long_first.p, lfirst.data(), lfirst.size() * 4, hipMemcpyHostToDevice, s));
-    GS_HIP(hipStreamSynchronize(s));
+    GS_HIP(hipStreamSynchronize(s));  // before the sort buffers are freed
     m.csr_planned = true;
 }
 

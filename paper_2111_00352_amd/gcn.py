@@ -153,7 +153,7 @@ def main():
     ap.add_argument("--epochs", type=int, default=10)
     ap.add_argument("--hidden", type=int, default=128)
     ap.add_argument("--out", type=int, default=64)
-    ap.add_argument("--lr", type=float, default=0.1)
+    ap.add_argument("--lr", type=float, default=0.02)
     a = ap.parse_args()
     sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
     import graphgen

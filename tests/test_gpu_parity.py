@@ -311,6 +311,24 @@ def test_csr_lane_shapes(monkeypatch, cpl, sort, F):
     check_spmm(case, case.build("csr"), X)
 
 
+@pytest.mark.parametrize("thr,chunk,wg", [(32, 32, 64), (16, 8, 100000), (200, 64, 201), (128, 128, 1024)])
+@pytest.mark.parametrize("sort", ["1", "2"])
+def test_csr_plan_thresholds(monkeypatch, thr, chunk, wg, sort):
+    # the device-built work plan under different long-row / chunk / workgroup
+    # thresholds: short, medium and huge rows in every mix, both row orders
+    monkeypatch.setenv("GS_CSR_LONG_ROW", str(thr))
+    monkeypatch.setenv("GS_CSR_CHUNK", str(chunk))
+    monkeypatch.setenv("GS_CSR_WG_ROW", str(wg))
+    monkeypatch.setenv("GS_CSR_SORT", sort)
+    g = graphgen.scaled(2)
+    case = _case_from_graph(g)
+    check_spmm(case, case.build("csr"), g.X[:, :64])
+    R, C = 700, 5000
+    row, col, val = graphgen.dense_rows_coo(R, C, [0, 3, 350, 699], seed=23, base_nnz=8000)
+    case = Case(R, C, row, col, val)
+    check_spmm(case, case.build("csr"), graphgen.features_x(C, 36, 24, "normal"))
+
+
 @pytest.mark.parametrize("F", [16, 48, 80, 512, 1040])
 def test_bsr16_matrix_core_widths(monkeypatch, F):
     # 16x16 blocks run on the matrix cores for F a multiple of 16 (wide F
