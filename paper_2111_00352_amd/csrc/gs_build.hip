@@ -486,12 +486,16 @@ __global__ __launch_bounds__(kTB) void k_bsr_to_coo(const int32_t *__restrict__ 
 
 // ------------------------------------------------------------ CSR -> COO
 
+// Row index of every entry: groups of 8 lanes per row, so a long row is
+// written by 8 lanes side by side and a wave covers 8 rows at once.
 __global__ __launch_bounds__(kTB) void k_expand_rows(const int32_t *__restrict__ rp, int64_t R,
                                                      int32_t *__restrict__ orow)
 {
-    for (int64_t i = (int64_t)blockIdx.x * kTB + threadIdx.x; i < R;
-         i += (int64_t)gridDim.x * kTB)
-        for (int64_t k = rp[i]; k < rp[i + 1]; k++) orow[k] = (int32_t)i;
+    constexpr int G = 8;
+    const int lane = threadIdx.x % G;
+    const int64_t groups = (int64_t)gridDim.x * (kTB / G);
+    for (int64_t i = ((int64_t)blockIdx.x * kTB + threadIdx.x) / G; i < R; i += groups)
+        for (int64_t k = rp[i] + lane; k < rp[i + 1]; k += G) orow[k] = (int32_t)i;
 }
 
 
@@ -714,7 +718,7 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
             m->col.alloc((size_t)Z * 4, s);
             m->val.alloc((size_t)Z * 4, s);
             if (Z) {
-                k_expand_rows<<<elem_grid(R), kTB, 0, s>>>(rp, R, m->row.as<int32_t>());
+                k_expand_rows<<<elem_grid(R * 8), kTB, 0, s>>>(rp, R, m->row.as<int32_t>());
                 GS_LAUNCH_CHECK();
                 GS_HIP(hipMemcpyAsync(m->col.p, col, (size_t)Z * 4, hipMemcpyDeviceToDevice, s));
                 GS_HIP(hipMemcpyAsync(m->val.p, val, (size_t)Z * 4, hipMemcpyDeviceToDevice, s));
@@ -728,7 +732,9 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
             mx.alloc(sizeof(int), s);
             GS_HIP(hipMemsetAsync(mx.p, 0, sizeof(int), s));
             if (R) {
-                k_max_row_len<<<elem_grid(R), kTB, 0, s>>>(rp, R, mx.as<int>());
+                // a few hundred workgroups: one atomic per wave on one word
+                k_max_row_len<<<(unsigned)std::min<int64_t>(256, ceil_div(R, kTB)), kTB, 0, s>>>(
+                    rp, R, mx.as<int>());
                 GS_LAUNCH_CHECK();
             }
             m->K = read_flag(mx.as<int>(), s);
@@ -756,7 +762,7 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
             wpos.alloc((size_t)(nw + 1) * 4, s);
             row.alloc((size_t)Z * 4, s);
             if (Z) {
-                k_expand_rows<<<elem_grid(R), kTB, 0, s>>>(rp, R, row.as<int32_t>());
+                k_expand_rows<<<elem_grid(R * 8), kTB, 0, s>>>(rp, R, row.as<int32_t>());
                 GS_LAUNCH_CHECK();
                 diag_bitmap(rp, col, R, C, Z, bm.as<uint32_t>(), s);
                 k_popc_words<<<elem_grid(nw), kTB, 0, s>>>(bm.as<uint32_t>(), nw, wpos.as<int32_t>());
@@ -848,7 +854,7 @@ void to_coo(const gs_matrix_ &m, int32_t *row, int32_t *col, float *val, hipStre
         GS_HIP(hipMemcpyAsync(val, m.val.p, (size_t)Z * 4, hipMemcpyDeviceToDevice, s));
         return;
     case GS_CSR:
-        k_expand_rows<<<elem_grid(R), kTB, 0, s>>>(m.row_ptr.as<int32_t>(), R, row);
+        k_expand_rows<<<elem_grid(R * 8), kTB, 0, s>>>(m.row_ptr.as<int32_t>(), R, row);
         GS_LAUNCH_CHECK();
         GS_HIP(hipMemcpyAsync(col, m.col.p, (size_t)Z * 4, hipMemcpyDeviceToDevice, s));
         GS_HIP(hipMemcpyAsync(val, m.val.p, (size_t)Z * 4, hipMemcpyDeviceToDevice, s));

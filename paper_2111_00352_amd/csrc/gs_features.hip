@@ -39,6 +39,81 @@ __global__ __launch_bounds__(kTB) void k_col_hist(const int32_t *__restrict__ co
         atomicAdd(&cc[col[k]], 1);
 }
 
+// Column counts without global atomics (large matrices): the column indices
+// are first bucketed by their high bits (windows of W = 2^shift columns, so a
+// window's counters fit in one workgroup's LDS), then every slice of a bucket
+// is counted by one workgroup in LDS and written out whole, and the slices'
+// counts are added per column.  Four passes over the indices in all.
+constexpr int kBucketTile = kTB * 16;  // indices per tile of the bucketing passes
+
+__global__ __launch_bounds__(kTB) void k_bucket_hist(const int32_t *__restrict__ col, int64_t Z,
+                                                     int shift, int nb, int64_t ntiles,
+                                                     int32_t *__restrict__ hist)
+{
+    __shared__ int h[256];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kBucketTile;
+    for (int i = 0; i < kBucketTile / kTB; i++) {
+        const int64_t k = base + (int64_t)i * kTB + threadIdx.x;
+        if (k < Z) atomicAdd(&h[col[k] >> shift], 1);
+    }
+    __syncthreads();
+    if (threadIdx.x < nb) hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
+}
+
+__global__ __launch_bounds__(kTB) void k_bucket_scatter(const int32_t *__restrict__ col, int64_t Z,
+                                                        int shift, int nb, int64_t ntiles,
+                                                        const int32_t *__restrict__ off,
+                                                        int32_t *__restrict__ out)
+{
+    __shared__ int run[256];
+    if (threadIdx.x < nb) run[threadIdx.x] = off[(int64_t)threadIdx.x * ntiles + blockIdx.x];
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kBucketTile;
+    for (int i = 0; i < kBucketTile / kTB; i++) {
+        const int64_t k = base + (int64_t)i * kTB + threadIdx.x;
+        if (k < Z) {
+            const int c = col[k];
+            out[atomicAdd(&run[c >> shift], 1)] = c;  // order inside a bucket is free
+        }
+    }
+}
+
+// Block (b, s): slice s of bucket b's indices, counted into W LDS counters.
+__global__ __launch_bounds__(kTB) void k_bucket_count(const int32_t *__restrict__ cols,
+                                                      const int32_t *__restrict__ off, int64_t ntiles,
+                                                      int shift, int slices,
+                                                      int32_t *__restrict__ partial)
+{
+    extern __shared__ int cnt[];
+    const int W = 1 << shift;
+    const int b = blockIdx.x / slices, sl = blockIdx.x % slices;
+    for (int j = threadIdx.x; j < W; j += kTB) cnt[j] = 0;
+    __syncthreads();
+    const int64_t b0 = off[(int64_t)b * ntiles], b1 = off[(int64_t)(b + 1) * ntiles];
+    const int64_t per = (b1 - b0 + slices - 1) / slices;
+    const int64_t k0 = b0 + sl * per, k1 = k0 + per < b1 ? k0 + per : b1;
+    const int cbase = b << shift;
+    for (int64_t k = k0 + threadIdx.x; k < k1; k += kTB) atomicAdd(&cnt[cols[k] - cbase], 1);
+    __syncthreads();
+    int32_t *out = partial + (int64_t)blockIdx.x * W;
+    for (int j = threadIdx.x; j < W; j += kTB) out[j] = cnt[j];
+}
+
+__global__ __launch_bounds__(kTB) void k_bucket_reduce(const int32_t *__restrict__ partial, int64_t C,
+                                                       int shift, int slices,
+                                                       int32_t *__restrict__ cc)
+{
+    const int64_t W = 1ll << shift;
+    for (int64_t c = (int64_t)blockIdx.x * kTB + threadIdx.x; c < C; c += (int64_t)gridDim.x * kTB) {
+        const int64_t b = c >> shift, j = c & (W - 1);
+        int sum = 0;
+        for (int s = 0; s < slices; s++) sum += partial[(b * slices + s) * W + j];
+        cc[c] = sum;
+    }
+}
+
 // Statistics of a count sequence cnt[i] = (ptr ? ptr[i+1]-ptr[i] : vals[i]).
 // Each workgroup reduces in registers, then across its waves in LDS, and
 // issues one set of atomics (the grid is kept small, so the few atomics on
@@ -187,7 +262,9 @@ __global__ __launch_bounds__(kTB) void k_mark_diags(const int32_t *__restrict__ 
         for (int64_t k = rp[i] + lane; k < rp[i + 1]; k += kWave) {
             int64_t sidx = (int64_t)col[k] - i + R - 1;
             const uint32_t bit = 1u << (sidx & 31);
-            if (!(__hip_atomic_load(&bm[sidx >> 5], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit))
+            // the check may read a stale copy cached near this workgroup:
+            // then the (idempotent) atomic is simply issued
+            if (!(__hip_atomic_load(&bm[sidx >> 5], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) & bit))
                 atomicOr(&bm[sidx >> 5], bit);
         }
     }
@@ -242,6 +319,42 @@ void diag_bitmap(const int32_t *rp, const int32_t *col, int64_t R, int64_t C, in
     }
 }
 
+// Column counts cc[0..C) (cleared here).  Bucketed LDS counting when the
+// matrix is large enough to pay for the extra passes, atomics otherwise.
+void column_counts(const int32_t *col, int64_t C, int64_t Z, int32_t *cc, hipStream_t s)
+{
+    int shift = 15;  // 32768 counters = 128 KiB of LDS
+    while (shift > 10 && ((int64_t)4 << shift) > max_lds_bytes()) shift--;
+    const int64_t nb = (C + (1ll << shift) - 1) >> shift;
+    if (Z < (1 << 20) || nb > 256 || std::getenv("GS_COLHIST_ATOMIC") != nullptr) {
+        GS_HIP(hipMemsetAsync(cc, 0, (size_t)C * 4, s));
+        if (Z > 0) {
+            k_col_hist<<<elem_grid(Z), kTB, 0, s>>>(col, Z, cc);
+            GS_HIP(hipGetLastError());
+        }
+        return;
+    }
+    const int64_t ntiles = ceil_div(Z, (int64_t)kBucketTile);
+    // about 512 workgroups in all (one at a time per CU at 128 KiB of LDS)
+    const int slices = (int)std::max<int64_t>(1, std::min<int64_t>(64, ceil_div(512, nb)));
+    DevBuf hist, sorted, partial;
+    hist.alloc((size_t)(nb * ntiles + 1) * 4, s);
+    sorted.alloc((size_t)Z * 4, s);
+    partial.alloc(((size_t)(nb * slices) << shift) * 4, s);
+    k_bucket_hist<<<(unsigned)ntiles, kTB, 0, s>>>(col, Z, shift, (int)nb, ntiles, hist.as<int32_t>());
+    GS_HIP(hipGetLastError());
+    exclusive_scan_i32(hist.as<int32_t>(), hist.as<int32_t>(), nb * ntiles, true, s);
+    k_bucket_scatter<<<(unsigned)ntiles, kTB, 0, s>>>(col, Z, shift, (int)nb, ntiles, hist.as<int32_t>(),
+                                                      sorted.as<int32_t>());
+    GS_HIP(hipGetLastError());
+    k_bucket_count<<<(unsigned)(nb * slices), kTB, (size_t)4 << shift, s>>>(
+        sorted.as<int32_t>(), hist.as<int32_t>(), ntiles, shift, slices, partial.as<int32_t>());
+    GS_HIP(hipGetLastError());
+    k_bucket_reduce<<<elem_grid(C), kTB, 0, s>>>(partial.as<int32_t>(), C, shift, slices, cc);
+    GS_HIP(hipGetLastError());
+    GS_HIP(hipStreamSynchronize(s));  // before the temporaries are freed
+}
+
 void features_from_csr(const gs_matrix_ &csr, hipStream_t s, gs_features *out)
 {
     const int64_t R = csr.R, C = csr.C, Z = csr.Z;
@@ -261,11 +374,7 @@ void features_from_csr(const gs_matrix_ &csr, hipStream_t s, gs_features *out)
     }
     if (C > 0) {
         cc.alloc((size_t)C * 4, s);
-        GS_HIP(hipMemsetAsync(cc.p, 0, (size_t)C * 4, s));
-        if (Z > 0) {
-            k_col_hist<<<elem_grid(Z), kTB, 0, s>>>(col, Z, cc.as<int32_t>());
-            GS_HIP(hipGetLastError());
-        }
+        column_counts(col, C, Z, cc.as<int32_t>(), s);
         k_count_stats<<<stats_grid(C), kTB, 0, s>>>(nullptr, cc.as<int32_t>(), C, 0, acc.as<FeatAcc>());
         GS_HIP(hipGetLastError());
     }

@@ -419,6 +419,16 @@ def test_diagonal_bitmap_paths_agree(monkeypatch, path):
         check_layout(case, "dia")
 
 
+@pytest.mark.parametrize("path", ["bucketed", "atomic"])
+def test_column_count_paths_agree(monkeypatch, path):
+    # bucketed LDS counting (over a million entries, several 32k-column
+    # windows, a ragged last window) and the atomic histogram give the same
+    # column features
+    if path == "atomic":
+        monkeypatch.setenv("GS_COLHIST_ATOMIC", "1")
+    check_features(_random_case(50_000, 70_001, 1_200_000, 95, empty=0.05))
+
+
 @pytest.mark.parametrize("merge", ["0", "1"])
 def test_block_count_kernels_agree(monkeypatch, merge):
     # the 16x16 block count (features, BSR sizing) has an LDS-bitmap kernel and
