@@ -419,8 +419,9 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
         const int64_t tiles = m.n_medium_rows + ceil_div(n_group_items, GPB);
         if (!tiles) return;
         if (n_huge) ensure_work(m, (size_t)m.n_long_chunks * F * 4, s);
-        // persistent grid: a few resident workgroups per CU
-        const int64_t cap = (int64_t)resident_workgroups() * env_int("GS_WG_MULT", 4);
+        // persistent grid: a few resident workgroups per CU (measured: 4 for
+        // length-sorted rows, 8 -- about one tile each -- for natural order)
+        const int64_t cap = (int64_t)resident_workgroups() * env_int("GS_WG_MULT", m.csr_sorted ? 4 : 8);
         dim3 grid((unsigned)std::max<int64_t>(1, std::min(tiles, cap / slices)), (unsigned)slices);
         k_csr_rows<CPL, G, FU><<<grid, kBlock, 0, s>>>(
             m.n_medium_rows, m.long_rows.as<int32_t>(), m.row_ptr.as<int32_t>(), m.csr_chunk,

@@ -181,9 +181,11 @@ bool dispatch_fast(const FastShape &sh, Fn &&fn)
     return false;
 }
 
+// Measured on the mesh and block workloads: 8 resident-workgroup multiples
+// (about one row tile per workgroup) beat a tighter persistent grid.
 unsigned persistent_grid(int64_t tiles, int64_t slices)
 {
-    const int64_t cap = (int64_t)resident_workgroups() * env_int("GS_WG_MULT", 2);
+    const int64_t cap = (int64_t)resident_workgroups() * env_int("GS_WG_MULT", 8);
     int64_t g = std::min(tiles, std::max<int64_t>(1, cap / std::max<int64_t>(1, slices)));
     return (unsigned)std::max<int64_t>(1, g);
 }
