@@ -166,7 +166,7 @@ def main():
     n0 = 256
     i0 = torch.arange(n0, dtype=torch.int32, device=dev)
     warm = gs.SelectContext("model")
-    for fmt_probe in ("csr", "coo", "ell", "dia", "bsr"):
+    for fmt_probe in ("csr", "coo", "ell", "dia", "bsr", "csc"):
         gs.build_format(i0, i0, torch.ones(n0, device=dev), (n0, n0), fmt_probe).spmm(
             torch.ones((n0, F), device=dev))
     warm.run(0, i0, i0, torch.ones(n0, device=dev), (n0, n0), torch.ones((n0, F), device=dev))
@@ -207,7 +207,7 @@ def main():
     # ---- per-launch duration of the chosen format's SpMM (HIP events on its stream)
     mats = {}
     fmt_rows = {}
-    for fmt in ("csr", "coo", "ell", "dia", "bsr"):
+    for fmt in ("csr", "coo", "ell", "dia", "bsr", "csc"):
         try:
             t0 = time.perf_counter()
             m = gs.build_format(row, col, val, (R, C), fmt)

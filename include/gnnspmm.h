@@ -4,7 +4,7 @@
  * The library computes Y = A.X, the neighbourhood aggregation of a GNN layer
  * (arXiv 2111.00352, Sec. 2.1: A is the sparse N x N adjacency, X the dense
  * N x d node-feature matrix), with A held in one of the sparse storage
- * formats of Sec. 2.2 (COO, CSR, DIA, BSR) or in padded row-packed ELL.
+ * formats of Sec. 2.2 (COO, CSR, CSC, DIA, BSR) or in padded row-packed ELL.
  * Around the kernels it provides what the paper's runtime does before each
  * GNN layer (Sec. 4, Sec. 4.6): extraction of the matrix features of Table 2
  * (Sec. 4.4), min-max normalisation and a tree-ensemble format predictor
@@ -45,7 +45,8 @@ typedef enum {
     GS_ELL = 2,
     GS_DIA = 3,
     GS_BSR = 4,
-    GS_NUM_FORMATS = 5
+    GS_CSC = 5,
+    GS_NUM_FORMATS = 6
 } gs_format;
 
 typedef enum {
@@ -101,6 +102,8 @@ int gs_set_allocator(const gs_allocator *a);
  * from it the requested layout, each in the canonical form:
  *   COO  row[nnz], col[nnz], val[nnz] sorted by (row, col)
  *   CSR  row_ptr[n_rows+1], col[nnz], val[nnz]
+ *   CSC  col_ptr[n_cols+1], row[nnz], val[nnz] sorted by (col, row): the
+ *        CSR of the transpose
  *   ELL  K = longest row; ell_col[K*n_rows], ell_val[K*n_rows], slot (i,k) at
  *        k*n_rows+i; padding col = -1, val = +0.0f
  *   DIA  offsets[N_diags] ascending distinct (col-row); data[N_diags*n_rows],
@@ -125,8 +128,13 @@ int gs_convert(gs_matrix A, int fmt, const gs_build_opts *opts, gs_stream s, gs_
  * X and Y must not overlap.  fp32 in and out; products and sums in fp32
  * (fused multiply-add), with every sequential chain kept short enough that
  * |Y - A.X| <= 1e-5 (|A|.|X|) + 1e-6 elementwise.  Deterministic: the same
- * inputs give bit-identical Y.  Fully asynchronous on s; the first call with
- * a larger F than before may allocate a workspace (in stream order). */
+ * inputs give bit-identical Y.  CSC is the exception: its columns scatter
+ * into the rows of Y, so the products (exact in fp64) are added with fp64
+ * atomics in a workspace and rounded to fp32 once; the order of the fp64
+ * additions varies, which can change an fp32 result only where an fp64
+ * sum sits on an fp32 rounding boundary.  Fully asynchronous on s; the
+ * first call with a larger F than before may allocate a workspace (in
+ * stream order). */
 int gs_spmm(gs_matrix A, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
             gs_stream s);
 
@@ -147,8 +155,9 @@ typedef struct {
 int gs_get_info(gs_matrix A, gs_matrix_info *info);
 
 /* Raw arrays of a built matrix, for inspection and bit-exact comparison.
- * which: 0 = row_ptr|row|ell_col|offsets|block_ptr, 1 = col|ell_val|data|block_col,
- *        2 = val|block_val (see gs_build_format for per-format meaning).
+ * which: 0 = row_ptr|row|ell_col|offsets|block_ptr|col_ptr,
+ *        1 = col|ell_val|data|block_col|row (CSC), 2 = val|block_val
+ *        (see gs_build_format for per-format meaning).
  * *dev_ptr receives a [dev] pointer owned by A, *bytes its size. */
 int gs_get_array(gs_matrix A, int which, const void **dev_ptr, uint64_t *bytes);
 
@@ -224,7 +233,7 @@ typedef struct {
     double t_features, t_predict, t_convert;
     int32_t chosen;
     int32_t feasible_mask;  /* bit f set if format f fits max_bytes */
-    double scores[5];       /* per-format predictor scores (MODEL) or seconds (PROFILE) */
+    double scores[GS_NUM_FORMATS]; /* per-format predictor scores (MODEL) or seconds (PROFILE) */
 } gs_select_stats;
 
 int gs_ctx_stats(gs_ctx c, gs_select_stats *out);
@@ -234,7 +243,7 @@ const char *gs_last_error(void);
 
 /* ABI version of this header (incremented on incompatible change). */
 int gs_abi_version(void);
-#define GS_ABI_VERSION 1
+#define GS_ABI_VERSION 2
 
 #ifdef __cplusplus
 }

@@ -9,7 +9,7 @@ The arithmetic lives in ``oracle.c`` (plain loops, fp64 SpMM accumulation);
 this module only compiles it with gcc and marshals numpy arrays.  Each wrapper
 names the passage of the paper (arXiv 2111.00352) it follows:
 
-* storage formats COO/CSR/DIA/BSR ............ Sec. 2.2 (ELL: padded row packing)
+* storage formats COO/CSR/CSC/DIA/BSR ........ Sec. 2.2 (ELL: padded row packing)
 * SpMM Y = A.X ................................ Sec. 2.1
 * features F1..F19 ............................ Sec. 4.4, Table 2
 * two-layer GCN forward / backward (gcn.py) ... Sec. 2.1, Sec. 5.1 (numpy fp64)
@@ -125,6 +125,13 @@ def csr(R, crow):
     rp = np.empty(R + 1, np.int32)
     lib().or_csr(R, crow.size, _p(crow), _p(rp))
     return rp
+
+
+def csc(R, C, row, col, val):
+    """CSC (Sec. 2.2): (col_ptr[C+1], row[Z], val[Z]) in (col, row) order --
+    by definition the CSR arrays of the transpose."""
+    ocol, orow, oval = canon(C, R, col, row, val)
+    return csr(C, ocol), orow, oval
 
 
 def ell(R, row_ptr, col, val):

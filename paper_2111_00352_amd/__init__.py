@@ -28,7 +28,7 @@ __all__ = [
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libgnnspmm.so")
 
-FORMATS = {"coo": 0, "csr": 1, "ell": 2, "dia": 3, "bsr": 4}
+FORMATS = {"coo": 0, "csr": 1, "ell": 2, "dia": 3, "bsr": 4, "csc": 5}
 FORMAT_NAMES = {v: k for k, v in FORMATS.items()}
 FEATURE_NAMES = [
     "numRow", "numCol", "NNZ", "N_diags", "aver_RD", "max_RD", "min_RD", "dev_RD",
@@ -69,7 +69,7 @@ class _SelOpts(ctypes.Structure):
 class _SelStats(ctypes.Structure):
     _fields_ = [("t_features", ctypes.c_double), ("t_predict", ctypes.c_double),
                 ("t_convert", ctypes.c_double), ("chosen", _i32), ("feasible_mask", _i32),
-                ("scores", ctypes.c_double * 5)]
+                ("scores", ctypes.c_double * len(FORMATS))]
 
 
 _ALLOC_FN = ctypes.CFUNCTYPE(_p, ctypes.c_size_t, _p, _p)
@@ -377,4 +377,4 @@ class SelectContext:
         _check(lib().gs_ctx_stats(self._h, ctypes.byref(st)))
         return dict(t_features=st.t_features, t_predict=st.t_predict, t_convert=st.t_convert,
                     chosen=FORMAT_NAMES.get(st.chosen, "?"), feasible_mask=st.feasible_mask,
-                    scores={FORMAT_NAMES[i]: st.scores[i] for i in range(5)})
+                    scores={FORMAT_NAMES[i]: st.scores[i] for i in range(len(FORMATS))})

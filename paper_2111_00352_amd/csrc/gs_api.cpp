@@ -65,6 +65,7 @@ void run_spmm(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
     case GS_ELL: spmm_ell(m, X, ldx, Y, ldy, F, s); break;
     case GS_DIA: spmm_dia(m, X, ldx, Y, ldy, F, s); break;
     case GS_BSR: spmm_bsr(m, X, ldx, Y, ldy, F, s); break;
+    case GS_CSC: spmm_csc(m, X, ldx, Y, ldy, F, s); break;
     default: fail(GS_ERR_INVALID_ARG, "corrupt matrix handle");
     }
 }

@@ -571,6 +571,36 @@ void radix_sort_pairs(uint64_t *ka, uint64_t *kb, uint32_t *pa, uint32_t *pb, in
     *perm = pin;
 }
 
+// Sorts the triplets (major[k], minor[k], val[k]) by (major, minor) into
+// omajor / ominor / oval (a stable LSD radix sort over the bits in use).
+// Used to move between row-major and column-major orders.
+void sort_triplets(const int32_t *major, const int32_t *minor, const float *val, int64_t Z,
+                   int64_t n_major, int64_t n_minor, int32_t *omajor, int32_t *ominor, float *oval,
+                   hipStream_t s)
+{
+    if (Z == 0) return;
+    std::vector<int> shifts;
+    for (int sft = 0; sft < bits_for(n_minor - 1); sft += 8) shifts.push_back(sft);
+    for (int sft = 0; sft < bits_for(n_major - 1); sft += 8) shifts.push_back(32 + sft);
+    DevBuf k0, k1, p0, p1, flags;
+    k0.alloc((size_t)Z * 8, s);
+    k1.alloc((size_t)Z * 8, s);
+    p0.alloc((size_t)Z * 4, s);
+    p1.alloc((size_t)Z * 4, s);
+    flags.alloc(sizeof(int), s);
+    GS_HIP(hipMemsetAsync(flags.p, 0, sizeof(int), s));
+    k_make_keys<<<elem_grid(Z), kTB, 0, s>>>(major, minor, Z, k0.as<uint64_t>());
+    GS_LAUNCH_CHECK();
+    uint64_t *keys = nullptr;
+    uint32_t *perm = nullptr;
+    radix_sort_pairs(k0.as<uint64_t>(), k1.as<uint64_t>(), p0.as<uint32_t>(), p1.as<uint32_t>(), Z,
+                     shifts, s, &keys, &perm);
+    k_unpack_sorted<<<elem_grid(Z), kTB, 0, s>>>(keys, perm, val, Z, omajor, ominor, oval,
+                                                 flags.as<int>());
+    GS_LAUNCH_CHECK();
+    GS_HIP(hipStreamSynchronize(s));  // before the sort buffers are freed
+}
+
 void canonicalize(const gs_coo &A, bool assume_canonical, hipStream_t s, CanonCOO &out)
 {
     const int64_t R = A.n_rows, C = A.n_cols, Z = A.nnz;
@@ -652,10 +682,10 @@ gs_matrix_ *csr_from_canon(CanonCOO &&c, hipStream_t s, bool plan)
 uint64_t format_bytes(int fmt, int64_t R, int64_t C, int64_t Z, int64_t K, int64_t ND, int64_t nb,
                       int b)
 {
-    (void)C;
     switch (fmt) {
     case GS_COO: return (uint64_t)Z * 12;
     case GS_CSR: return (uint64_t)(R + 1) * 4 + (uint64_t)Z * 8;
+    case GS_CSC: return (uint64_t)(C + 1) * 4 + (uint64_t)Z * 8;
     case GS_ELL: return (uint64_t)K * (uint64_t)R * 8;
     case GS_DIA: return (uint64_t)ND * 4 + (uint64_t)ND * (uint64_t)R * 4;
     case GS_BSR: {
@@ -709,6 +739,27 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
             }
             m->device_bytes = need;
             plan_csr(*m, s);
+            break;
+        }
+        case GS_CSC: {
+            uint64_t need = format_bytes(GS_CSC, R, C, Z, 0, 0, 0, 0);
+            if (bytes_required) *bytes_required = need;
+            m->row_ptr.alloc((size_t)(C + 1) * 4, s);
+            m->col.alloc((size_t)Z * 4, s);
+            m->val.alloc((size_t)Z * 4, s);
+            DevBuf rows, cols;
+            rows.alloc((size_t)Z * 4, s);
+            cols.alloc((size_t)Z * 4, s);
+            if (Z) {
+                k_expand_rows<<<elem_grid(R * 8), kTB, 0, s>>>(rp, R, rows.as<int32_t>());
+                GS_LAUNCH_CHECK();
+                sort_triplets(col, rows.as<int32_t>(), val, Z, C, R, cols.as<int32_t>(),
+                              m->col.as<int32_t>(), m->val.as<float>(), s);
+            }
+            k_row_ptr<<<elem_grid(Z + 1), kTB, 0, s>>>(cols.as<int32_t>(), Z, C, m->row_ptr.as<int32_t>());
+            GS_LAUNCH_CHECK();
+            GS_HIP(hipStreamSynchronize(s));  // before rows / cols are freed
+            m->device_bytes = need;
             break;
         }
         case GS_COO: {
@@ -859,6 +910,15 @@ void to_coo(const gs_matrix_ &m, int32_t *row, int32_t *col, float *val, hipStre
         GS_HIP(hipMemcpyAsync(col, m.col.p, (size_t)Z * 4, hipMemcpyDeviceToDevice, s));
         GS_HIP(hipMemcpyAsync(val, m.val.p, (size_t)Z * 4, hipMemcpyDeviceToDevice, s));
         return;
+    case GS_CSC: {  // back to (row, col) order
+        DevBuf cols;
+        cols.alloc((size_t)Z * 4, s);
+        k_expand_rows<<<elem_grid(C * 8), kTB, 0, s>>>(m.row_ptr.as<int32_t>(), C, cols.as<int32_t>());
+        GS_LAUNCH_CHECK();
+        sort_triplets(m.col.as<int32_t>(), cols.as<int32_t>(), m.val.as<float>(), Z, R, C, row, col,
+                      val, s);
+        return;
+    }
     default: break;
     }
     DevBuf pos;

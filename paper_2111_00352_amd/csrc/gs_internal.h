@@ -93,7 +93,9 @@ struct gs_matrix_ {
     int64_t R = 0, C = 0, Z = 0;
     hipStream_t stream = nullptr;  // stream the arrays were allocated on
 
-    // COO (row, col, val) and CSR (row_ptr, col, val) share col/val.
+    // COO (row, col, val) and CSR (row_ptr, col, val) share col/val; CSC
+    // keeps its col_ptr / row indices / values in row_ptr / col / val (it is
+    // the CSR of the transpose).
     gs::DevBuf row, row_ptr, col, val;
     // ELL
     int64_t K = 0;
@@ -220,6 +222,8 @@ void spmm_ell(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
 void spmm_dia(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
               hipStream_t s);
 void spmm_bsr(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+              hipStream_t s);
+void spmm_csc(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
               hipStream_t s);
 
 // Plans built at conversion time for the CSR and COO kernels.

@@ -142,7 +142,8 @@ int gs_get_array(gs_matrix A, int which, const void **dev_ptr, uint64_t *bytes)
     const DevBuf *b = nullptr;
     switch (A->fmt) {
     case GS_COO: b = which == 0 ? &A->row : which == 1 ? &A->col : &A->val; break;
-    case GS_CSR: b = which == 0 ? &A->row_ptr : which == 1 ? &A->col : &A->val; break;
+    case GS_CSR:
+    case GS_CSC: b = which == 0 ? &A->row_ptr : which == 1 ? &A->col : &A->val; break;
     case GS_ELL:
         if (which == 2) {
             set_error("gs_get_array: ELL has arrays 0 (ell_col) and 1 (ell_val)");

@@ -175,7 +175,7 @@ void score(const Model &m, const double *x, double *sc)
 }
 
 // Tie order when scores or times are equal.
-constexpr int kTieOrder[GS_NUM_FORMATS] = {GS_CSR, GS_COO, GS_ELL, GS_DIA, GS_BSR};
+constexpr int kTieOrder[GS_NUM_FORMATS] = {GS_CSR, GS_COO, GS_ELL, GS_DIA, GS_BSR, GS_CSC};
 
 double now_s()
 {
@@ -184,7 +184,7 @@ double now_s()
 
 struct Entry {
     gs_features feat{};
-    gs_matrix_ *built[GS_NUM_FORMATS] = {nullptr, nullptr, nullptr, nullptr, nullptr};
+    gs_matrix_ *built[GS_NUM_FORMATS] = {};
     uint64_t bytes[GS_NUM_FORMATS] = {0};
     int feasible = 0;
     std::unordered_map<int64_t, int> profiled;  // F -> fastest format
@@ -228,7 +228,7 @@ Entry &lookup(gs_ctx_ &c, uint64_t key, const gs_coo *A, hipStream_t s)
         const gs_features &f = e->feat;
         for (int fmt = 0; fmt < GS_NUM_FORMATS; fmt++) {
             e->bytes[fmt] = format_bytes(fmt, f.n_rows, f.n_cols, f.nnz, f.max_rd, f.n_diags, nb, b);
-            if (fmt == GS_CSR || fmt == GS_COO || e->bytes[fmt] <= c.opts.max_bytes)
+            if (fmt == GS_CSR || fmt == GS_COO || fmt == GS_CSC || e->bytes[fmt] <= c.opts.max_bytes)
                 e->feasible |= 1 << fmt;
         }
         e->t_features = now_s() - t0;

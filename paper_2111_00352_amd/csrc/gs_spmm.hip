@@ -301,6 +301,48 @@ __global__ __launch_bounds__(kBlock) void k_coo_fixup(const int4 *__restrict__ s
     }
 }
 
+// ---------------------------------------------------------------- CSC
+// Column j of A scatters a_ij * X[j,:] into row i of Y for each of its
+// entries, so rows are summed by many workgroups at once.  The products are
+// exact in fp64 (24-bit mantissas), they are added with fp64 atomics into a
+// workspace W (R x F doubles), and W is rounded to Y once: the fp64 sums
+// carry no error that matters at fp32, whatever their order.  One wave per
+// column, lanes over the F columns of X.
+
+__global__ __launch_bounds__(kBlock) void k_fill_f64(double *__restrict__ w, int64_t n)
+{
+    for (int64_t k = (int64_t)blockIdx.x * kBlock + threadIdx.x; k < n;
+         k += (int64_t)gridDim.x * kBlock)
+        w[k] = 0.0;
+}
+
+__global__ __launch_bounds__(kBlock) void k_csc_scatter(int64_t C, const int32_t *__restrict__ cp,
+                                                        const int32_t *__restrict__ ri,
+                                                        const float *__restrict__ val,
+                                                        const float *__restrict__ X, int64_t ldx,
+                                                        int64_t F, double *__restrict__ W)
+{
+    const int lane = threadIdx.x % kWave;
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    for (int64_t j = ((int64_t)blockIdx.x * kBlock + threadIdx.x) / kWave; j < C; j += waves) {
+        const int32_t k0 = cp[j], k1 = cp[j + 1];
+        if (k0 == k1) continue;
+        for (int64_t c = lane; c < F; c += kWave) {
+            const double x = (double)X[j * ldx + c];
+            for (int32_t k = k0; k < k1; k++)
+                unsafeAtomicAdd(&W[(int64_t)ri[k] * F + c], (double)val[k] * x);
+        }
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_round_f64(const double *__restrict__ W, int64_t R,
+                                                      int64_t F, float *__restrict__ Y, int64_t ldy)
+{
+    for (int64_t k = (int64_t)blockIdx.x * kBlock + threadIdx.x; k < R * F;
+         k += (int64_t)gridDim.x * kBlock)
+        Y[(k / F) * ldy + k % F] = (float)W[k];
+}
+
 // ---------------------------------------------------------------- ELL
 // One group per row; slot (i,k) lives at k*R + i, so for a fixed k the
 // groups of a block read consecutive addresses.  Padding (col = -1) ends
@@ -604,6 +646,28 @@ void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
             GS_HIP(hipGetLastError());
         }
     });
+}
+
+void spmm_csc(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+              hipStream_t s)
+{
+    const int64_t n = m.R * F;
+    if (n == 0) return;
+    ensure_work(m, (size_t)n * 8, s);
+    double *W = m.work.as<double>();
+    auto grid = [](int64_t items) {
+        int64_t g = ceil_div(items, (int64_t)kBlock);
+        return (unsigned)(g < 1 ? 1 : g > 65536 ? 65536 : g);
+    };
+    k_fill_f64<<<grid(n), kBlock, 0, s>>>(W, n);
+    GS_HIP(hipGetLastError());
+    if (m.Z) {
+        k_csc_scatter<<<grid(m.C * kWave), kBlock, 0, s>>>(m.C, m.row_ptr.as<int32_t>(), m.col.as<int32_t>(),
+                                                             m.val.as<float>(), X, ldx, F, W);
+        GS_HIP(hipGetLastError());
+    }
+    k_round_f64<<<grid(n), kBlock, 0, s>>>(W, m.R, F, Y, ldy);
+    GS_HIP(hipGetLastError());
 }
 
 void spmm_ell(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,

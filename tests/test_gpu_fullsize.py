@@ -15,7 +15,7 @@ import paper_2111_00352_amd as gs
 
 pytestmark = pytest.mark.gpu
 
-FMTS = ["csr", "coo", "ell", "dia", "bsr"]
+FMTS = ["csr", "coo", "ell", "dia", "bsr", "csc"]
 
 
 class Full:

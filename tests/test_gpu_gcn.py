@@ -98,7 +98,7 @@ def test_gcn_training_agrees_across_formats():
     g, X, W1, W2, T = _problem(3, 32, 16, 4500)
     args = (_dev(g.row), _dev(g.col), _dev(g.val), (g.R, g.C))
     curves = {}
-    for mode in ("model", "fixed:csr", "fixed:coo", "fixed:ell", "fixed:dia", "fixed:bsr"):
+    for mode in ("model", "fixed:csr", "fixed:coo", "fixed:ell", "fixed:dia", "fixed:bsr", "fixed:csc"):
         name, _, fixed = mode.partition(":")
         ctx = gs.SelectContext(name, fixed=fixed or "csr")
         adj = gcn.Adjacency(*args, ctx, key=21, symmetric=False)

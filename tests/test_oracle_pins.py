@@ -48,6 +48,8 @@ def test_w1_layouts():
     assert bp.tolist() == g["bsr_block_ptr"]
     assert bc.tolist() == g["bsr_block_col"]
     assert bv.tolist() == g["bsr_block_val"]
+    cp, cr, cv = oracle.csc(R, C, row[::-1], col[::-1], val[::-1])
+    assert cp.tolist() == g["csc_col_ptr"] and cr.tolist() == g["csc_row"] and cv.tolist() == g["csc_val"]
 
 
 def test_w1_padding_is_positive_zero():
@@ -385,3 +387,19 @@ def test_mesh_generator_matches_grid():
     n, row, col = _grid(512)
     assert (g.row == row).all() and (g.col == col).all()
     assert (g.val > 0).all() and (g.val <= 1).all()
+
+
+@pytest.mark.parametrize("R,C,nnz,seed", [(40, 25, 200, 3), (7, 90, 60, 4), (64, 64, 0, 5)])
+def test_csc_is_the_column_compressed_dense_matrix(R, C, nnz, seed):
+    # brute force: walking the dense matrix column by column, top to bottom
+    row, col, val = graphgen.random_coo(R, C, nnz, seed, empty_rows=0.2)
+    cp, cr, cv = oracle.csc(R, C, *graphgen.shuffled(row, col, val, seed + 1))
+    A = _dense(R, C, row, col, val)
+    exp_ptr, exp_row, exp_val = [0], [], []
+    for j in range(C):
+        nz = np.nonzero(A[:, j])[0]
+        exp_row += nz.tolist()
+        exp_val += A[nz, j].tolist()
+        exp_ptr.append(exp_ptr[-1] + nz.size)
+    assert cp.tolist() == exp_ptr and cr.tolist() == exp_row
+    assert np.array_equal(cv.astype(np.float64), np.array(exp_val, dtype=np.float64))
