@@ -205,6 +205,8 @@ typedef struct {
     uint64_t max_bytes;     /* formats whose padded size exceeds this are never chosen; 0 -> 8 GiB */
     int32_t bsr_block;      /* 0 -> 16 */
     int32_t profile_reps;   /* timed runs per format for GS_SEL_PROFILE; 0 -> 3 */
+    uint32_t formats;       /* candidates of MODEL and PROFILE: bit f set = gs_format f;
+                               0 -> every format (the paper's whole pool) */
 } gs_selector_opts;
 
 int gs_ctx_create(const gs_selector_opts *o, gs_ctx *out);

@@ -276,7 +276,7 @@ int choose(gs_ctx_ &c, Entry &e, int64_t F, const float *X, int64_t ldx, float *
         score(c.model, x, sc);
         double best = -1e300;
         for (int fmt : kTieOrder) {
-            if (!(e.feasible & (1 << fmt))) continue;
+            if (!(e.feasible & c.opts.formats & (1u << fmt))) continue;
             for (int k = 0; k < c.model.k; k++)
                 if (c.model.cls_fmt[k] == fmt) {
                     st.scores[fmt] = sc[k];
@@ -300,7 +300,7 @@ int choose(gs_ctx_ &c, Entry &e, int64_t F, const float *X, int64_t ldx, float *
             double best = 1e300;
             try {
                 for (int fmt : kTieOrder) {
-                    if (!(e.feasible & (1 << fmt))) continue;
+                    if (!(e.feasible & c.opts.formats & (1u << fmt))) continue;
                     gs_matrix_ &m = ensure_built(c, e, fmt, s);
                     run_spmm(m, X, ldx, Y, ldy, F, s);  // warm-up (and workspace growth)
                     GS_HIP(hipEventRecord(a, s));
@@ -323,6 +323,7 @@ int choose(gs_ctx_ &c, Entry &e, int64_t F, const float *X, int64_t ldx, float *
             }
             (void)hipEventDestroy(a);
             (void)hipEventDestroy(b);
+            if (chosen < 0) chosen = GS_CSR;  // no feasible candidate: the fallback
             e.profiled[F] = chosen;
         }
         for (int f = 0; f < GS_NUM_FORMATS; f++) st.scores[f] = e.prof_time[f];
@@ -343,8 +344,11 @@ int gs_ctx_create(const gs_selector_opts *o, gs_ctx *out)
     if (out) *out = nullptr;
     return guarded([&] {
         if (!out) fail(GS_ERR_INVALID_ARG, "null output handle");
-        gs_selector_opts r = {GS_SEL_MODEL, GS_CSR, nullptr, kDefaultMaxBytes, kDefaultBsrBlock, 3};
+        gs_selector_opts r = {GS_SEL_MODEL, GS_CSR, nullptr, kDefaultMaxBytes, kDefaultBsrBlock, 3, 0};
         if (o) r = *o;
+        constexpr uint32_t kAll = (1u << GS_NUM_FORMATS) - 1;
+        if (r.formats == 0) r.formats = kAll;
+        if (r.formats & ~kAll) fail(GS_ERR_INVALID_ARG, "candidate mask names an unknown format");
         if (r.mode < GS_SEL_MODEL || r.mode > GS_SEL_FIXED) fail(GS_ERR_INVALID_ARG, "bad selector mode");
         if (r.fixed < 0 || r.fixed >= GS_NUM_FORMATS) fail(GS_ERR_INVALID_ARG, "bad fixed format");
         if (r.max_bytes == 0) r.max_bytes = kDefaultMaxBytes;

@@ -34,7 +34,7 @@ def profile(n, row, col, val, F, key, reps):
     r, c, v = (torch.from_numpy(a).to(dev) for a in (row, col, val))
     X = torch.randn(n, F, device=dev)
     feats = gs.extract_features(r, c, v, (n, n))
-    ctx = gs.SelectContext("profile", profile_reps=reps)
+    ctx = gs.SelectContext("profile", profile_reps=reps, formats=FMT)
     ctx.run(key, r, c, v, (n, n), X)
     st = ctx.stats()
     ctx.close()
@@ -48,10 +48,13 @@ def main():
     ap.add_argument("--random", type=int, default=300)
     ap.add_argument("--structured", type=int, default=120)
     ap.add_argument("--reps", type=int, default=5)
+    ap.add_argument("--start", type=int, default=0, help="first job (to split a collection)")
+    ap.add_argument("--count", type=int, default=None, help="number of jobs from --start")
     a = ap.parse_args()
     torch.cuda.set_device(0)
     jobs = [("random", i, (64, 128)) for i in range(a.random)]
     jobs += [("structured", i, (64, 128, 256)) for i in range(a.structured)]
+    jobs = jobs[a.start:None if a.count is None else a.start + a.count]
     t0 = time.time()
     with open(a.out, "w", newline="") as fh:
         w = csv.writer(fh)

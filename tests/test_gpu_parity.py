@@ -391,6 +391,18 @@ def test_select_and_run_modes(mode):
     assert oracle.check_spmm(_host(Y2), Yref2, M2)[0]
 
 
+@pytest.mark.parametrize("mode", ["model", "profile"])
+def test_select_respects_candidate_formats(mode):
+    g = graphgen.scaled(3)
+    case = _case_from_graph(g)
+    ctx = gs.SelectContext(mode, formats=["coo", "ell"])
+    Y, chosen = ctx.run(5, case.d_row, case.d_col, case.d_val, (case.R, case.C), _dev(g.X))
+    assert chosen in ("coo", "ell")
+    Yref, M = oracle.spmm(case.R, case.rp, case.ccol, case.cval, g.X)
+    assert oracle.check_spmm(_host(Y), Yref, M)[0]
+    ctx.close()
+
+
 def test_select_model_on_mesh_prefers_diagonals():
     g = graphgen.scaled(3)
     case = _case_from_graph(g)

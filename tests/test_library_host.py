@@ -143,3 +143,12 @@ def test_trained_model_export_matches_sklearn(tmp_path):
     trees, base, classes = train.export(clf, mn, mx, str(tmp_path / "m.gsm"))
     S = train.score_exported(trees, base, Xn)
     assert (np.array([classes[i] for i in S.argmax(axis=1)]) == clf.predict(Xn)).all()
+
+
+def test_candidate_mask_is_checked(L):
+    o = gs._SelOpts(0, 1, None, 0, 16, 3, 1 << 7)  # bit 7 names no format
+    h = ctypes.c_void_p()
+    assert L.gs_ctx_create(ctypes.byref(o), ctypes.byref(h)) == gs.ERR_INVALID_ARG
+    o = gs._SelOpts(0, 1, None, 0, 16, 3, (1 << 1) | (1 << 5))  # CSR and CSC only
+    assert L.gs_ctx_create(ctypes.byref(o), ctypes.byref(h)) == 0
+    L.gs_ctx_destroy(h)
