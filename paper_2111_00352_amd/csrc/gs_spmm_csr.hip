@@ -322,7 +322,6 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
     const int wg_thr = env_int("GS_CSR_WG_ROW", kCsrWgRow);
     m.csr_long_thr = thr;
     m.csr_chunk = chunk;
-    m.csr_wg_thr = wg_thr;
     const int64_t R = m.R;
     const int32_t *rp = m.row_ptr.as<int32_t>();
 
@@ -344,7 +343,18 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
     if (force == 1) sorted = false;
     if (force == 2) sorted = true;
     m.csr_sorted = sorted;
-    const int64_t n_long = st.n_long, n_huge = st.n_huge;
+    // A workgroup per medium row pays off for a few hub rows running beside
+    // the short ones; with more medium rows than resident workgroups they
+    // would queue behind each other with most of each workgroup idle, so then
+    // every long row is cut into chunk items instead.
+    int wg_thr_eff = wg_thr;
+    int64_t n_huge = st.n_huge;
+    if (st.n_long - st.n_huge > resident_workgroups()) {
+        wg_thr_eff = thr;
+        n_huge = st.n_long;
+    }
+    m.csr_wg_thr = wg_thr_eff;
+    const int64_t n_long = st.n_long;
     m.n_long_rows = n_long;
     m.n_medium_rows = n_long - n_huge;
     m.n_short = R - n_long;
@@ -357,7 +367,7 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
         kb.alloc((size_t)R * 8, s);
         pa.alloc((size_t)R * 4, s);
         pb.alloc((size_t)R * 4, s);
-        k_plan_keys<<<plan_grid(R), kBlock, 0, s>>>(rp, R, thr, wg_thr, sorted ? 1 : 0, st.maxlen,
+        k_plan_keys<<<plan_grid(R), kBlock, 0, s>>>(rp, R, thr, wg_thr_eff, sorted ? 1 : 0, st.maxlen,
                                                     ka.as<uint64_t>());
         GS_HIP(hipGetLastError());
         std::vector<int> shifts;
@@ -400,10 +410,14 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
 {
     auto al = [](const void *p) { return ((uintptr_t)p % 16) == 0; };
     if (F % 4 || ldx % 4 || ldy % 4 || !al(X) || !al(Y)) return false;
-    // Lane shape: skewed (length-sorted) matrices gather rows at random, and
-    // there wide groups (32 lanes, one X row per half-wave) do best; rows in
-    // natural order do best with 16 columns per lane (more rows per wave).
-    int cpl = env_int("GS_CSR_CPL", m.csr_sorted ? (int)std::max<int64_t>(4, std::min<int64_t>(16, F / 32)) : 16);
+    // Lane shape, measured over 160 profiled matrices at F = 64..256: four
+    // columns per lane (wide groups, 8 X rows in flight per lane) is best or
+    // near it, except in natural row order for very short rows (fewer than 8
+    // entries on average) and for wide X (F >= 256) with rows under 64
+    // entries, where 16 columns per lane -- more rows per wave -- wins.
+    const bool many_rows_per_wave =
+        !m.csr_sorted && (m.Z < 8 * m.R || (F >= 256 && m.Z < 64 * m.R));
+    int cpl = env_int("GS_CSR_CPL", many_rows_per_wave ? 16 : 4);
     if (cpl != 4 && cpl != 8 && cpl != 16) cpl = 16;
     while (cpl > 4 && F < 4 * (int64_t)cpl) cpl /= 2;  // at least 4 lanes per group
     const int64_t lanes = ceil_div(F, cpl);
