@@ -222,6 +222,13 @@ Entry &lookup(gs_ctx_ &c, uint64_t key, const gs_coo *A, hipStream_t s)
         gs_build_opts o = {c.opts.bsr_block, 0, c.opts.max_bytes};
         gs_matrix_ *csr = build_csr(A, o, s, false);  // planned when CSR is first run
         e->built[GS_CSR] = csr;
+        if (c.opts.mode == GS_SEL_FIXED) {
+            // a fixed format needs no features: its build reports whether it fits
+            e->feasible = (1 << GS_NUM_FORMATS) - 1;
+            e->t_features = now_s() - t0;
+            c.cache[key] = e;
+            return *e;
+        }
         features_from_csr(*csr, s, &e->feat);
         const int b = c.opts.bsr_block;
         const int64_t nb = (b == 16) ? e->feat.n_blocks16 : count_blocks(*csr, b, s);

@@ -129,3 +129,25 @@ def test_gcn_end_to_end_reports_every_mode():
     for m in ("model", "fixed:csr", "fixed:coo"):
         assert res[m]["total_s"] > 0 and np.isfinite(res[m]["final_loss"])
     assert res["speedup_model_vs_fixed:csr"] > 0
+
+
+@pytest.mark.parametrize("mode", ["model", "fixed:csr", "fixed:coo", "fixed:dia"])
+def test_gcn_graph_replays_match_eager(mode):
+    # a captured training step replayed for the later epochs gives the same
+    # losses and weights, bit for bit, as running every epoch eagerly (the
+    # kernels and their order are the same); each replay is checked, with an
+    # eager synchronisation between replays
+    torch.backends.cuda.matmul.allow_tf32 = False
+    g, X, W1, W2, T = _problem(3, 32, 16, 4700)
+    args = (_dev(g.row), _dev(g.col), _dev(g.val), (g.R, g.C))
+    name, _, fixed = mode.partition(":")
+    out = {}
+    for graph in (False, True):
+        ctx = gs.SelectContext(name, fixed=fixed or "csr")
+        adj = gcn.Adjacency(*args, ctx, key=31, symmetric=False)
+        model, losses, _ = gcn.train(adj, _dev(X), _dev(T), _dev(W1), _dev(W2), epochs=6, lr=0.05,
+                                     graph=graph)
+        out[graph] = (losses, model.W1.detach().cpu().numpy(), model.W2.detach().cpu().numpy())
+        ctx.close()
+    assert out[True][0] == out[False][0]
+    assert np.array_equal(out[True][1], out[False][1]) and np.array_equal(out[True][2], out[False][2])

@@ -391,6 +391,17 @@ def test_select_and_run_modes(mode):
     assert oracle.check_spmm(_host(Y2), Yref2, M2)[0]
 
 
+def test_fixed_selector_reports_an_infeasible_format():
+    # the fixed mode extracts no features; the build itself reports the cap
+    g = graphgen.scaled(2)
+    case = _case_from_graph(g)
+    ctx = gs.SelectContext("fixed", fixed="dia", max_bytes=1 << 20)
+    with pytest.raises(gs.GnnSpmmError) as e:
+        ctx.run(9, case.d_row, case.d_col, case.d_val, (case.R, case.C), _dev(g.X[:, :16]))
+    assert e.value.code == gs.ERR_INFEASIBLE
+    ctx.close()
+
+
 @pytest.mark.parametrize("mode", ["model", "profile"])
 def test_select_respects_candidate_formats(mode):
     g = graphgen.scaled(3)
