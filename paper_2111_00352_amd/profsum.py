@@ -27,8 +27,11 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 
 
 def source_hash() -> str:
+    """Hash of the device code: the HIP sources and the headers they include
+    (host-only .cpp files -- ABI glue, selector -- do not change a kernel)."""
     h = hashlib.sha256()
-    for p in sorted(glob.glob(os.path.join(HERE, "csrc", "*"))):
+    files = glob.glob(os.path.join(HERE, "csrc", "*.hip")) + glob.glob(os.path.join(HERE, "csrc", "*.h"))
+    for p in sorted(files):
         with open(p, "rb") as f:
             h.update(os.path.basename(p).encode())
             h.update(f.read())
