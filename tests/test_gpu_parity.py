@@ -333,7 +333,12 @@ def test_csr_plan_thresholds(monkeypatch, thr, chunk, wg, sort):
     R, C = 700, 5000
     row, col, val = graphgen.dense_rows_coo(R, C, [0, 3, 350, 699], seed=23, base_nnz=8000)
     case = Case(R, C, row, col, val)
-    check_spmm(case, case.build("csr"), graphgen.features_x(C, 36, 24, "normal"))
+    m = case.build("csr")
+    check_spmm(case, m, graphgen.features_x(C, 36, 24, "normal"))
+    # several column slices (one completion count per huge row and slice),
+    # then a narrower call on the same handle
+    check_spmm(case, m, graphgen.features_x(C, 300, 25, "normal"))
+    check_spmm(case, m, graphgen.features_x(C, 20, 26, "normal"))
 
 
 @pytest.mark.parametrize("F", [16, 48, 80, 512, 1040])
