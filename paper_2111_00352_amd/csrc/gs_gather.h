@@ -10,17 +10,11 @@
 
 namespace gs {
 
-// Gathered X rows: plain cached loads (GS_X_LOAD_POLICY selects an
-// alternative cache policy when the library is built for experiments).
+// Gathered X rows: plain cached loads (non-temporal loads measured slower:
+// hub rows are reused from L2 and the MALL).
 __device__ __forceinline__ float4 load_x4(const float *p)
 {
-#if defined(GS_X_LOAD_POLICY) && GS_X_LOAD_POLICY == 1
-    typedef float f4v __attribute__((ext_vector_type(4)));
-    const f4v v = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(p));
-    return make_float4(v[0], v[1], v[2], v[3]);
-#else
     return *reinterpret_cast<const float4 *>(p);
-#endif
 }
 
 // One batch of B entries j .. j+B-1 of the group's current index batch:

@@ -66,22 +66,33 @@ def short(name: str) -> str:
     return name.split("(")[0] if "(" in name else name
 
 
+def picked(name: str, kernels) -> bool:
+    """True when the kernel's name (template arguments included, without the
+    return type and namespace) is one of `kernels`."""
+    return short(str(name)).split("gs::")[-1] in kernels
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace")
     ap.add_argument("--fetch")
     ap.add_argument("--write")
-    ap.add_argument("--kernel", default="k_csr_items")
+    ap.add_argument("--kernel", default="k_csr_rows<4, 32, true>;k_csr_combine<4, 32>",
+                    help="kernel names (with template arguments) of one SpMM, separated by ;")
     ap.add_argument("--calib-bytes", type=float, default=256 * 2**20)
     ap.add_argument("--traffic-json")
+    ap.add_argument("--counters", nargs="*", default=[],
+                    help="further --pmc runs: every counter averaged per dispatch of the --kernel kernels")
+    ap.add_argument("--top", type=int, default=25, help="kernels listed from the trace (by total time)")
     ap.add_argument("--cmd", default="")
     a = ap.parse_args()
+    kernels = [k.strip() for k in a.kernel.split(";")]
     if a.cmd:
         print(f"command: {a.cmd}")
     if a.trace:
         kt = kernel_times(a.trace)
         print(f"{'dispatches':>10} {'avg_us':>10} {'median_us':>10} {'min_us':>10}  kernel")
-        for name, ds in sorted(kt.items(), key=lambda kv: -sum(kv[1])):
+        for name, ds in sorted(kt.items(), key=lambda kv: -sum(kv[1]))[:a.top]:
             ds = sorted(ds)
             print(f"{len(ds):10d} {sum(ds) / len(ds):10.2f} {ds[len(ds) // 2]:10.2f} {ds[0]:10.2f}  {short(name)}")
     out = {}
@@ -98,10 +109,23 @@ def main():
                 continue
             avg = sum(v) / len(v)
             print(f"  {len(v):5d}x {avg:14.1f} KiB  {short(str(kn))}")
-            if a.kernel in str(kn) and factor:
+            if picked(kn, kernels) and factor:
                 out[label] = out.get(label, 0.0) + avg * 1024.0 * factor
         if factor:
             out[f"{label}_factor"] = factor
+    for path in a.counters:
+        c = counters(path)
+        print(f"\ncounters of *{a.kernel}* kernels (average per dispatch): {os.path.basename(os.path.dirname(path))}")
+        per = collections.defaultdict(dict)
+        for (kn, cn), v in sorted(c.items()):
+            if picked(kn, kernels):
+                per[short(str(kn))][cn] = sum(v) / len(v)
+        for kn, cs in per.items():
+            line = "  ".join(f"{cn}={val:.4g}" for cn, val in sorted(cs.items()))
+            hit, miss = cs.get("TCC_HIT_sum"), cs.get("TCC_MISS_sum")
+            if hit is not None and miss is not None and hit + miss > 0:
+                line += f"  L2 hit rate={hit / (hit + miss):.3f}"
+            print(f"  {kn}: {line}")
     if a.traffic_json and "fetch" in out and "write" in out:
         out["bytes"] = out["fetch"] + out["write"]
         out["kernel"] = a.kernel
