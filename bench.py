@@ -61,25 +61,36 @@ def time_launches(fn, stream, reps, inputs):
 
 
 def cpu_baseline(g, F, budget_s=10.0):
+    """The oracle's SpMM on this host: all threads for about budget_s, then
+    one thread for a quarter of that (the results are identical)."""
     import oracle
 
     rp = oracle.csr(g.R, g.row)
     X = g.X[:, :F]
-    t0 = time.perf_counter()
-    reps = 0
-    while True:
-        oracle.spmm(g.R, rp, g.col, g.val, X)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s:
-            break
-    flops = 2.0 * g.nnz * F * reps
+
+    def rate(budget):
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            oracle.spmm(g.R, rp, g.col, g.val, X)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget:
+                return 2.0 * g.nnz * F * reps / el / 1e9, reps, el
+
+    threads = oracle.num_threads()
+    v, reps, el = rate(budget_s)
+    oracle.set_threads(1)
+    v1, reps1, el1 = rate(budget_s / 4)
+    oracle.set_threads(threads)
     return {
-        "value": round(flops / el / 1e9, 3),
+        "value": round(v, 3),
         "unit": "GFLOP/s",
-        "cores": oracle.num_threads(),
+        "cores": threads,
         "kind": "oracle",
-        "sample": f"full {g.R}-row SpMM (fp64 accumulation, plus |A||X|) repeated {reps}x in {el:.1f}s",
+        "sample": f"full {g.R}-row SpMM (fp64 accumulation, plus |A||X|) repeated {reps}x in {el:.1f}s "
+                  f"on {threads} threads; single thread: {reps1}x in {el1:.1f}s",
+        "single_thread_value": round(v1, 3),
     }
 
 
@@ -275,6 +286,9 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
+            # measured bytes over the same launch time: the rate the memory
+            # system actually sustains for this kernel
+            "traffic_rate_gbs": None if traffic is None else round(traffic * 1e6 / t_sel / 1e9, 1),
             "traffic_unit": "MB per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "bytes_per_launch": balg,
             "launch_us": round(t_sel * 1e6, 2),
@@ -301,6 +315,9 @@ def main():
         "formats": fmt_rows,
         "gen_s": round(t_gen, 2),
         "device": torch.cuda.get_device_name(0),
+        "arch": getattr(torch.cuda.get_device_properties(0), "gcnArchName", None),
+        "compute_units": torch.cuda.get_device_properties(0).multi_processor_count,
+        "hip": torch.version.hip,
     }
     if not args.no_gcn:
         out["gcn_e2e"] = gcn_e2e(g, row, col, val, Xs[0], args)

@@ -90,7 +90,8 @@ typedef struct {
     void *ctx;
 } gs_allocator;
 
-typedef struct gs_matrix_ *gs_matrix; /* opaque; owns its device arrays; immutable once built */
+typedef struct gs_matrix_ *gs_matrix; /* opaque; owns its device arrays (the format's arrays are
+                                         immutable once built) and one SpMM workspace */
 typedef struct gs_ctx_ *gs_ctx;       /* opaque; per-adjacency feature/format cache + selector */
 
 /* Installs the device allocator for all later allocations (NULL restores
@@ -134,7 +135,10 @@ int gs_convert(gs_matrix A, int fmt, const gs_build_opts *opts, gs_stream s, gs_
  * additions varies, which can change an fp32 result only where an fp64
  * sum sits on an fp32 rounding boundary.  Fully asynchronous on s; the
  * first call with a larger F than before may allocate a workspace (in
- * stream order). */
+ * stream order).  That workspace (partial sums of split rows, COO carries,
+ * the CSC accumulator) belongs to the handle: SpMM calls on one handle must
+ * not overlap in time (issue them on one stream or order them); different
+ * handles are independent. */
 int gs_spmm(gs_matrix A, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
             gs_stream s);
 

@@ -79,6 +79,7 @@ def lib():
             "or_spmm_rows": (ctypes.c_int, [i64, p, p, p, p, p, i64, i64, p, p]),
             "or_spmm64": (ctypes.c_int, [i64, p, p, p, p, i64, i64, p]),
             "or_num_threads": (ctypes.c_int, []),
+            "or_set_threads": (None, [ctypes.c_int]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -243,6 +244,11 @@ def spmm_rows(rows, row_ptr, col, val, X):
 
 def num_threads() -> int:
     return int(lib().or_num_threads())
+
+
+def set_threads(n: int) -> None:
+    """Thread count of the parallel SpMM loop (results are identical for any n)."""
+    lib().or_set_threads(int(n))
 
 
 def spmm_bound(M):

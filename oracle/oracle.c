@@ -457,3 +457,14 @@ int or_num_threads(void)
     return 1;
 #endif
 }
+
+/* Threads of later parallel loops (timing only; results do not depend on it:
+ * every row is summed by one thread in one fixed order). */
+void or_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
