@@ -56,6 +56,37 @@ def labels(T):
     return np.array(out)  # index into TIE_ORDER
 
 
+def footprints(path):
+    """Device bytes of every candidate format per sample (TIE_ORDER), from the
+    profiled matrix's integer features -- the memory term M of Eq. 1.  Same
+    sizes the library allocates: CSR 4(R+1)+8Z, COO 12Z, ELL 8 R max_RD,
+    DIA 4 N_diags (R+1), BSR16 4(ceil(R/16)+1) + 1036 n_blocks16."""
+    with open(path) as fh:
+        rows = list(csv.DictReader(fh))
+    M = []
+    for r in rows:
+        R, Z = float(r["numRow"]), float(r["NNZ"])
+        nb, nd, k = float(r["n_blocks16"]), float(r["N_diags"]), float(r["max_RD"])
+        M.append([4 * (R + 1) + 8 * Z, 12 * Z, 8 * R * k, 4 * nd * (R + 1),
+                  4 * (math.ceil(R / 16) + 1) + (4 + 8 + 1024) * nb])
+    return np.array(M)
+
+
+def labels_eq1(T, M, w, tie=1e-4):
+    """Eq. 1: the format minimising w R + (1 - w) M, with running time R and
+    memory footprint M scaled to [0, 1] by the min and max over the whole
+    profiled training set; formats within `tie` of the minimum count as
+    optimal (Fig. 5 caption) and the earliest in TIE_ORDER is taken."""
+    ok = np.isfinite(T)
+    tmin, tmax = T[ok].min(), T[ok].max()
+    mmin, mmax = M[ok].min(), M[ok].max()
+    Tf, Mf = np.where(ok, T, tmin), np.where(ok, M, mmin)
+    O = w * (Tf - tmin) / (tmax - tmin) + (1.0 - w) * (Mf - mmin) / (mmax - mmin)
+    O = np.where(ok, O, np.inf)
+    best = O.min(axis=1, keepdims=True)
+    return np.argmax(O <= best + tie, axis=1)
+
+
 def normalise(X, mn, mx):
     span = mx - mn
     Z = np.where(span > 0, (X - mn) / np.where(span > 0, span, 1), 0.0)
@@ -134,15 +165,50 @@ def evaluate(T, pred):
     return sp, frac, orac, int((~ok).sum())
 
 
+def cross_validate(X, y, groups, folds):
+    from sklearn.model_selection import GroupKFold
+
+    pred = np.zeros_like(y)
+    for tr, te in GroupKFold(n_splits=folds).split(X, y, groups):
+        mn, mx = X[tr].min(axis=0), X[tr].max(axis=0)
+        pred[te] = fit(normalise(X[tr], mn, mx), y[tr]).predict(normalise(X[te], mn, mx))
+    return pred
+
+
+def w_sweep(a, X, T, groups, ws):
+    """Sec. 6.5, impact of the optimisation goal: per w, the label mix and
+    the cross-validated accuracy of a model trained for that w."""
+    M = footprints(a.data)
+    lines = [f"Eq. 1 labels per w on {len(X)} profiled samples ({len(set(groups))} matrices), "
+             f"{a.folds}-fold grouped cross-validation "
+             f"(`python -m paper_2111_00352_amd.selector.train --w-sweep ...`).", "",
+             "| w | " + " | ".join(TIE_ORDER) + " | accuracy |", "|---" * (len(TIE_ORDER) + 2) + "|"]
+    for w in ws:
+        y = labels_eq1(T, M, w)
+        counts = [int((y == c).sum()) for c in range(len(TIE_ORDER))]
+        acc = float((cross_validate(X, y, groups, a.folds) == y).mean()) if len(set(y)) > 1 else 1.0
+        print(f"w={w:.2f} labels " + ", ".join(f"{f}={n}" for f, n in zip(TIE_ORDER, counts))
+              + f"  accuracy {acc:.3f}", flush=True)
+        lines.append(f"| {w:.2f} | " + " | ".join(str(n) for n in counts) + f" | {acc:.3f} |")
+    if a.md:
+        with open(a.md, "w") as fh:
+            fh.write("\n".join(lines) + "\n")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("data", nargs="?", default=DATA_PATH)
     ap.add_argument("--out", default=MODEL_PATH)
     ap.add_argument("--folds", type=int, default=5)
+    ap.add_argument("--w-sweep", help="comma-separated w values of Eq. 1: cross-validate a model per w "
+                                      "(labels from time and memory) instead of exporting one")
+    ap.add_argument("--md", help="with --w-sweep: also write the table as markdown")
     a = ap.parse_args()
     from sklearn.model_selection import GroupKFold
 
     X, T, groups, kinds = load(a.data)
+    if a.w_sweep:
+        return w_sweep(a, X, T, groups, [float(v) for v in a.w_sweep.split(",")])
     y = labels(T)
     print(f"{len(y)} samples, {len(set(groups))} matrices; label counts: "
           + ", ".join(f"{TIE_ORDER[c]}={int((y == c).sum())}" for c in range(5)))

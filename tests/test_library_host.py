@@ -152,3 +152,32 @@ def test_candidate_mask_is_checked(L):
     o = gs._SelOpts(0, 1, None, 0, 16, 3, (1 << 1) | (1 << 5))  # CSR and CSC only
     assert L.gs_ctx_create(ctypes.byref(o), ctypes.byref(h)) == 0
     L.gs_ctx_destroy(h)
+
+
+def test_eq1_labels_trade_time_for_memory():
+    # Eq. 1 over min-max scaled time and memory: w = 1 picks the fastest
+    # format, w = 0 the smallest, an infeasible (inf time) format never wins,
+    # and near-equal objectives go to the earliest format in the tie order
+    import numpy as np
+    from paper_2111_00352_amd.selector import train
+    inf = np.inf
+    T = np.array([[2.0, 1.0, 3.0, inf, 4.0],     # fastest: coo (index 1)
+                  [1.0, 1.0, 5.0, 6.0, 7.0]])    # csr and coo tie on time
+    M = np.array([[5.0, 9.0, 1.0, 0.5, 8.0],     # smallest feasible: ell (the inf-time dia is out)
+                  [3.0, 3.0, 9.0, 9.0, 9.0]])
+    assert train.labels_eq1(T, M, 1.0).tolist() == [1, 0]
+    assert train.labels_eq1(T, M, 0.0).tolist() == [2, 0]
+    mid = train.labels_eq1(T, M, 0.5).tolist()
+    assert mid[1] == 0 and mid[0] in (0, 1, 2)
+
+
+def test_footprints_match_the_library_sizes():
+    # M of Eq. 1 on the shipped profiles: the CSR and COO sizes follow from
+    # the row and entry counts alone
+    import numpy as np
+    from paper_2111_00352_amd.selector import DATA_PATH, train
+    M = train.footprints(DATA_PATH)
+    assert M.shape[1] == 5 and np.all(M[:, 0] > 0)
+    X, T, _, _ = train.load(DATA_PATH)
+    R, Z = X[:, 0], X[:, 2]
+    assert np.allclose(M[:, 0], 4 * (R + 1) + 8 * Z) and np.allclose(M[:, 1], 12 * Z)
