@@ -59,7 +59,7 @@ typedef enum {
     GS_ERR_OOM = -6,           /* the allocator returned NULL */
     GS_ERR_HIP = -7,           /* a HIP runtime call failed */
     GS_ERR_MODEL = -8,         /* predictor model missing or malformed */
-    GS_ERR_UNSUPPORTED = -9    /* a valid request this build does not handle */
+    GS_ERR_UNSUPPORTED = -9    /* a valid request the library does not handle */
 } gs_status;
 
 /* A sparse matrix in coordinate form, as PyTorch-Geometric hands it over
