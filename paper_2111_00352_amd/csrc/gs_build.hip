@@ -250,6 +250,24 @@ __global__ __launch_bounds__(kTB) void k_ell_to_coo(const int32_t *__restrict__ 
 // Diagonal d of the R x C matrix has offset col - row in [-(R-1), C-1];
 // slot index sidx = offset + R - 1.  A bitmap marks the occupied ones.
 
+// Number of BSR blocks with at least `thr` stored columns (per-workgroup sum,
+// then one atomic).
+__global__ __launch_bounds__(kTB) void k_count_dense(const uint64_t *__restrict__ mask, int64_t nb,
+                                                     int thr, unsigned long long *__restrict__ out)
+{
+    __shared__ unsigned long long part[kTB / kWave];
+    unsigned long long n = 0;
+    for (int64_t k = (int64_t)blockIdx.x * kTB + threadIdx.x; k < nb; k += (int64_t)gridDim.x * kTB)
+        n += __popcll(mask[k]) >= thr;
+    n = wave_sum_u64(n);
+    if (lane_id() == 0) part[threadIdx.x / kWave] = n;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < kTB / kWave; w++) n += part[w];
+        if (n) atomicAdd(out, n);
+    }
+}
+
 __global__ __launch_bounds__(kTB) void k_popc_words(const uint32_t *__restrict__ bm, int64_t nw,
                                                     int32_t *__restrict__ cnt)
 {
@@ -874,12 +892,16 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
                     m->bval.as<float>(), m->bmask.as<uint64_t>());
                 GS_LAUNCH_CHECK();
                 // dense-block count (kernel choice at SpMM time)
-                std::vector<uint64_t> hm((size_t)nb);
-                GS_HIP(hipMemcpyAsync(hm.data(), m->bmask.p, (size_t)nb * 8, hipMemcpyDeviceToHost, s));
+                DevBuf dn;
+                dn.alloc(sizeof(unsigned long long), s);
+                GS_HIP(hipMemsetAsync(dn.p, 0, sizeof(unsigned long long), s));
+                k_count_dense<<<(unsigned)std::min<int64_t>(1024, ceil_div(nb, (int64_t)kTB)), kTB, 0, s>>>(
+                    m->bmask.as<uint64_t>(), nb, kBsrDenseCols, dn.as<unsigned long long>());
+                GS_LAUNCH_CHECK();
+                unsigned long long dense = 0;
+                GS_HIP(hipMemcpyAsync(&dense, dn.p, sizeof dense, hipMemcpyDeviceToHost, s));
                 GS_HIP(hipStreamSynchronize(s));
-                int64_t dense = 0;
-                for (uint64_t x : hm) dense += __builtin_popcountll(x) >= kBsrDenseCols;
-                m->n_dense_blocks = dense;
+                m->n_dense_blocks = (int64_t)dense;
             }
             m->device_bytes = need;
             break;

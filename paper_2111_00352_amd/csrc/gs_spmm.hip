@@ -155,8 +155,9 @@ __global__ __launch_bounds__(kBlock) void k_csr_combine(const int32_t *__restric
 
 // ---------------------------------------------------------------- COO
 // Segmented reduction over the (row, col)-sorted triplets.  Group q owns
-// entries [bounds[q], bounds[q+1]): whole rows packed up to CH entries, or
-// one CH-entry piece of a row longer than CH.  Row boundaries inside the
+// entries [bounds[q], bounds[q+1]): the whole rows that start in one window
+// of CH entry positions (at most 2*CH - 1 entries), or one CH-entry piece of
+// a row longer than CH.  Row boundaries inside the
 // chunk are found with a ballot over "row differs from the previous entry";
 // a segment is written straight to Y unless its row continues into a
 // neighbouring chunk (only a split row does), in which case its partial
@@ -544,53 +545,176 @@ int env_int_coo(const char *name, int dflt)
 
 // --------------------------------------------------------------- plans
 
-// COO chunks follow row boundaries: whole rows are packed into chunks of at
-// most `chunk` entries, and only a row longer than that is cut into chunk-
-// sized pieces (whose partial sums the fixup launch adds).  Also lists the
-// empty rows, which the kernel must zero.
+// COO chunks follow row boundaries.  The chunk bounds are the sorted,
+// de-duplicated union of (a) for every window [q*CH, (q+1)*CH) of entry
+// positions, the first row start at or after q*CH, and (b) for every row
+// longer than CH, its start, end and CH-entry piece boundaries.  A chunk
+// then holds the whole rows that start in one window (at most 2*CH - 1
+// entries, every row at most CH) or one piece of a long row, whose partial
+// sums the fixup launch adds.  Also lists the split rows and the empty rows,
+// which the kernel must zero.  Built on the device: counts, scans, one radix
+// sort, compactions.
+
+namespace {
+
+constexpr int kPB = 256;
+
+inline unsigned plan_blocks(int64_t n)
+{
+    int64_t g = ceil_div(n, (int64_t)kPB);
+    return (unsigned)(g < 1 ? 1 : g > 8192 ? 8192 : g);
+}
+
+// Smallest i in [0, n) with a[i] >= t, or n.
+__device__ __forceinline__ int64_t lower_bound_i32(const int32_t *a, int64_t n, int64_t t)
+{
+    int64_t lo = 0, hi = n;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (a[mid] < t)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+__global__ __launch_bounds__(kPB) void k_coo_row_counts(const int32_t *__restrict__ rp, int64_t R, int chunk,
+                                                        int32_t *__restrict__ cand, int32_t *__restrict__ is_long,
+                                                        int32_t *__restrict__ is_empty)
+{
+    for (int64_t i = (int64_t)blockIdx.x * kPB + threadIdx.x; i < R; i += (int64_t)gridDim.x * kPB) {
+        const int len = rp[i + 1] - rp[i];
+        const bool lg = len > chunk;
+        cand[i] = lg ? (len + chunk - 1) / chunk + 1 : 0;  // start, piece boundaries, end
+        is_long[i] = lg;
+        is_empty[i] = len == 0;
+    }
+}
+
+__global__ __launch_bounds__(kPB) void k_coo_window_cands(const int32_t *__restrict__ rp, int64_t R, int64_t Z,
+                                                          int chunk, int64_t W, uint64_t *__restrict__ keys)
+{
+    for (int64_t q = (int64_t)blockIdx.x * kPB + threadIdx.x; q < W; q += (int64_t)gridDim.x * kPB) {
+        const int64_t t = q * chunk;
+        const int64_t i = t > Z ? R + 1 : lower_bound_i32(rp, R + 1, t);
+        keys[q] = (uint64_t)(i <= R ? rp[i] : Z);
+    }
+}
+
+__global__ __launch_bounds__(kPB) void k_coo_long_cands(const int32_t *__restrict__ rp, int64_t R, int chunk,
+                                                        const int32_t *__restrict__ coff, int64_t W,
+                                                        uint64_t *__restrict__ keys)
+{
+    for (int64_t i = (int64_t)blockIdx.x * kPB + threadIdx.x; i < R; i += (int64_t)gridDim.x * kPB) {
+        const int n = coff[i + 1] - coff[i];
+        const int64_t s0 = rp[i], e = rp[i + 1];
+        for (int k = 0; k < n; k++) {
+            const int64_t b = s0 + (int64_t)k * chunk;
+            keys[W + coff[i] + k] = (uint64_t)(b < e ? b : e);
+        }
+    }
+}
+
+__global__ __launch_bounds__(kPB) void k_flag_new(const uint64_t *__restrict__ keys, int64_t n,
+                                                  int32_t *__restrict__ flag)
+{
+    for (int64_t k = (int64_t)blockIdx.x * kPB + threadIdx.x; k < n; k += (int64_t)gridDim.x * kPB)
+        flag[k] = k == 0 || keys[k] != keys[k - 1];
+}
+
+__global__ __launch_bounds__(kPB) void k_compact_bounds(const uint64_t *__restrict__ keys, int64_t n,
+                                                        const int32_t *__restrict__ off,
+                                                        int32_t *__restrict__ bounds)
+{
+    for (int64_t k = (int64_t)blockIdx.x * kPB + threadIdx.x; k < n; k += (int64_t)gridDim.x * kPB)
+        if (off[k + 1] > off[k]) bounds[off[k]] = (int32_t)keys[k];
+}
+
+__global__ __launch_bounds__(kPB) void k_coo_lists(const int32_t *__restrict__ rp, int64_t R, int chunk,
+                                                   const int32_t *__restrict__ loff,
+                                                   const int32_t *__restrict__ eoff,
+                                                   const int32_t *__restrict__ bounds, int64_t nbnd,
+                                                   int4 *__restrict__ split, int32_t *__restrict__ empty)
+{
+    for (int64_t i = (int64_t)blockIdx.x * kPB + threadIdx.x; i < R; i += (int64_t)gridDim.x * kPB) {
+        if (loff[i + 1] > loff[i]) {
+            const int len = rp[i + 1] - rp[i];
+            const int64_t first = lower_bound_i32(bounds, nbnd, rp[i]);  // rp[i] is a bound
+            split[loff[i]] = make_int4((int)i, (int)first, (len + chunk - 1) / chunk, 0);
+        }
+        if (eoff[i + 1] > eoff[i]) empty[eoff[i]] = (int32_t)i;
+    }
+}
+
+}  // namespace
+
 void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s)
 {
     const int chunk = env_int_coo("GS_COO_CHUNK", kCooChunk);
     m.coo_chunk = chunk;
-    std::vector<int32_t> rp((size_t)m.R + 1);
-    GS_HIP(hipMemcpyAsync(rp.data(), row_ptr, rp.size() * 4, hipMemcpyDeviceToHost, s));
-    GS_HIP(hipStreamSynchronize(s));
-    std::vector<int32_t> empty, bounds{0};
-    std::vector<int4> split;
-    int64_t cur = 0;
-    for (int64_t i = 0; i < m.R; i++) {
-        const int32_t pos = rp[i], len = rp[i + 1] - rp[i];
-        if (len == 0) {
-            empty.push_back((int32_t)i);
-            continue;
-        }
-        if (len > chunk) {
-            if (pos > bounds.back()) bounds.push_back(pos);
-            split.push_back(make_int4((int)i, (int)bounds.size() - 1, (len + chunk - 1) / chunk, 0));
-            for (int32_t o = chunk; o < len; o += chunk) bounds.push_back(pos + o);
-            bounds.push_back(pos + len);
-            cur = 0;
-            continue;
-        }
-        if (cur + len > chunk) {
-            bounds.push_back(pos);
-            cur = 0;
-        }
-        cur += len;
+    const int64_t R = m.R, Z = m.Z;
+    DevBuf cand, lng, emp;
+    cand.alloc((size_t)(R + 1) * 4, s);
+    lng.alloc((size_t)(R + 1) * 4, s);
+    emp.alloc((size_t)(R + 1) * 4, s);
+    if (R > 0) {
+        k_coo_row_counts<<<plan_blocks(R), kPB, 0, s>>>(row_ptr, R, chunk, cand.as<int32_t>(),
+                                                         lng.as<int32_t>(), emp.as<int32_t>());
+        GS_HIP(hipGetLastError());
     }
-    if (m.Z > bounds.back()) bounds.push_back((int32_t)m.Z);
-    m.n_coo_chunks = (int64_t)bounds.size() - 1;
-    m.n_coo_split = (int64_t)split.size();
-    m.n_empty_rows = (int64_t)empty.size();
-    m.coo_bounds.alloc(bounds.size() * 4, s);
-    m.coo_split.alloc(split.size() * sizeof(int4), s);
-    m.empty_rows.alloc(empty.size() * 4, s);
-    GS_HIP(hipMemcpyAsync(m.coo_bounds.p, bounds.data(), bounds.size() * 4, hipMemcpyHostToDevice, s));
-    if (!split.empty())
-        GS_HIP(hipMemcpyAsync(m.coo_split.p, split.data(), split.size() * sizeof(int4), hipMemcpyHostToDevice, s));
-    if (!empty.empty())
-        GS_HIP(hipMemcpyAsync(m.empty_rows.p, empty.data(), empty.size() * 4, hipMemcpyHostToDevice, s));
+    exclusive_scan_i32(cand.as<int32_t>(), cand.as<int32_t>(), R, true, s);
+    exclusive_scan_i32(lng.as<int32_t>(), lng.as<int32_t>(), R, true, s);
+    exclusive_scan_i32(emp.as<int32_t>(), emp.as<int32_t>(), R, true, s);
+    int32_t tot[3] = {0, 0, 0};
+    GS_HIP(hipMemcpyAsync(&tot[0], cand.as<int32_t>() + R, 4, hipMemcpyDeviceToHost, s));
+    GS_HIP(hipMemcpyAsync(&tot[1], lng.as<int32_t>() + R, 4, hipMemcpyDeviceToHost, s));
+    GS_HIP(hipMemcpyAsync(&tot[2], emp.as<int32_t>() + R, 4, hipMemcpyDeviceToHost, s));
     GS_HIP(hipStreamSynchronize(s));
+
+    const int64_t W = ceil_div(Z, (int64_t)chunk) + 1;  // the last window starts at or past Z
+    const int64_t n = W + tot[0];
+    DevBuf ka, kb, pa, pb, flag;
+    ka.alloc((size_t)n * 8, s);
+    kb.alloc((size_t)n * 8, s);
+    pa.alloc((size_t)n * 4, s);
+    pb.alloc((size_t)n * 4, s);
+    flag.alloc((size_t)(n + 1) * 4, s);
+    k_coo_window_cands<<<plan_blocks(W), kPB, 0, s>>>(row_ptr, R, Z, chunk, W, ka.as<uint64_t>());
+    GS_HIP(hipGetLastError());
+    if (tot[0]) {
+        k_coo_long_cands<<<plan_blocks(R), kPB, 0, s>>>(row_ptr, R, chunk, cand.as<int32_t>(), W,
+                                                         ka.as<uint64_t>());
+        GS_HIP(hipGetLastError());
+    }
+    std::vector<int> shifts;
+    for (int sft = 0; sft < bits_for(Z); sft += 8) shifts.push_back(sft);
+    uint64_t *keys = nullptr;
+    uint32_t *perm = nullptr;
+    radix_sort_pairs(ka.as<uint64_t>(), kb.as<uint64_t>(), pa.as<uint32_t>(), pb.as<uint32_t>(), n, shifts, s,
+                     &keys, &perm);
+    k_flag_new<<<plan_blocks(n), kPB, 0, s>>>(keys, n, flag.as<int32_t>());
+    GS_HIP(hipGetLastError());
+    exclusive_scan_i32(flag.as<int32_t>(), flag.as<int32_t>(), n, true, s);
+    int32_t nbnd = 0;
+    GS_HIP(hipMemcpyAsync(&nbnd, flag.as<int32_t>() + n, 4, hipMemcpyDeviceToHost, s));
+    GS_HIP(hipStreamSynchronize(s));
+
+    m.n_coo_chunks = nbnd - 1;
+    m.n_coo_split = tot[1];
+    m.n_empty_rows = tot[2];
+    m.coo_bounds.alloc((size_t)nbnd * 4, s);
+    m.coo_split.alloc((size_t)tot[1] * sizeof(int4), s);
+    m.empty_rows.alloc((size_t)tot[2] * 4, s);
+    k_compact_bounds<<<plan_blocks(n), kPB, 0, s>>>(keys, n, flag.as<int32_t>(), m.coo_bounds.as<int32_t>());
+    GS_HIP(hipGetLastError());
+    if (R > 0 && (tot[1] || tot[2])) {
+        k_coo_lists<<<plan_blocks(R), kPB, 0, s>>>(row_ptr, R, chunk, lng.as<int32_t>(), emp.as<int32_t>(),
+                                                   m.coo_bounds.as<int32_t>(), nbnd, m.coo_split.as<int4>(),
+                                                   m.empty_rows.as<int32_t>());
+        GS_HIP(hipGetLastError());
+    }
+    GS_HIP(hipStreamSynchronize(s));  // before the temporaries are freed
 }
 
 // --------------------------------------------------------------- launchers
