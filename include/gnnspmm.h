@@ -82,8 +82,12 @@ typedef struct {
 } gs_build_opts;
 
 /* Optional device allocator (e.g. PyTorch's caching allocator).  alloc must
- * return memory usable on the given stream, or NULL.  NULL hooks (the
- * default) mean hipMalloc / hipFree. */
+ * return memory usable on the given stream, or NULL.  The hooks must be
+ * stream-ordered: free(p, s) can be called while work already enqueued on s
+ * still uses p, so p may go to later work on s, but to other streams only
+ * once that work has completed (PyTorch's caching allocator and
+ * hipFreeAsync behave so).  NULL hooks (the default) mean hipMalloc and a
+ * synchronisation of s before hipFree. */
 typedef struct {
     void *(*alloc)(size_t bytes, gs_stream s, void *ctx);
     void (*free)(void *p, gs_stream s, void *ctx);

@@ -246,27 +246,50 @@ __global__ __launch_bounds__(kTB) void k_ell_to_coo(const int32_t *__restrict__ 
     }
 }
 
-// ------------------------------------------------------------------- DIA
-// Diagonal d of the R x C matrix has offset col - row in [-(R-1), C-1];
-// slot index sidx = offset + R - 1.  A bitmap marks the occupied ones.
-
-// Number of BSR blocks with at least `thr` stored columns (per-workgroup sum,
-// then one atomic).
-__global__ __launch_bounds__(kTB) void k_count_dense(const uint64_t *__restrict__ mask, int64_t nb,
-                                                     int thr, unsigned long long *__restrict__ out)
+// Sum of cnt[0..n) (k_sum_counts) and number of BSR blocks with at least
+// `thr` stored columns (k_count_dense): one partial per workgroup, or, from a
+// one-workgroup grid, the result itself added to *out.
+__global__ __launch_bounds__(kTB) void k_sum_counts(const int32_t *__restrict__ cnt, int64_t n,
+                                                    unsigned long long *__restrict__ part,
+                                                    unsigned long long *__restrict__ out)
 {
-    __shared__ unsigned long long part[kTB / kWave];
+    __shared__ unsigned long long t64[kTB / kWave];
+    unsigned long long t = 0;
+    for (int64_t k = (int64_t)blockIdx.x * kTB + threadIdx.x; k < n; k += (int64_t)gridDim.x * kTB)
+        t += (unsigned long long)cnt[k];
+    t = block_sum_u64<kTB>(t, t64);
+    if (threadIdx.x != 0) return;
+    if (gridDim.x == 1)
+        *out += t;
+    else
+        part[blockIdx.x] = t;
+}
+
+__global__ __launch_bounds__(kTB) void k_count_dense(const uint64_t *__restrict__ mask, int64_t nb,
+                                                     int thr, unsigned long long *__restrict__ part,
+                                                     unsigned long long *__restrict__ out)
+{
+    __shared__ unsigned long long t64[kTB / kWave];
     unsigned long long n = 0;
     for (int64_t k = (int64_t)blockIdx.x * kTB + threadIdx.x; k < nb; k += (int64_t)gridDim.x * kTB)
         n += __popcll(mask[k]) >= thr;
-    n = wave_sum_u64(n);
-    if (lane_id() == 0) part[threadIdx.x / kWave] = n;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        for (int w = 1; w < kTB / kWave; w++) n += part[w];
-        if (n) atomicAdd(out, n);
-    }
+    n = block_sum_u64<kTB>(n, t64);
+    if (threadIdx.x != 0) return;
+    if (gridDim.x == 1)
+        *out += n;
+    else
+        part[blockIdx.x] = n;
 }
+
+inline unsigned reduce_grid(int64_t n)
+{
+    int64_t g = ceil_div(n, (int64_t)kTB * 4);
+    return (unsigned)(g < 1 ? 1 : g > 2048 ? 2048 : g);
+}
+
+// ------------------------------------------------------------------- DIA
+// Diagonal d of the R x C matrix has offset col - row in [-(R-1), C-1];
+// slot index sidx = offset + R - 1.  A bitmap marks the occupied ones.
 
 __global__ __launch_bounds__(kTB) void k_popc_words(const uint32_t *__restrict__ bm, int64_t nw,
                                                     int32_t *__restrict__ cnt)
@@ -414,6 +437,81 @@ __global__ __launch_bounds__(kTB) void k_bsr_count_lds(const int32_t *__restrict
     }
 }
 
+// BSR fill with a bitmap of block columns in LDS, one workgroup per block
+// row (persistent).  The block row's entries mark their block columns; an
+// exclusive prefix of the bitmap words' populations numbers the blocks in
+// column order (block j of the row is the j-th set bit), which gives bcol
+// and, for every entry, its block: the entries are placed in parallel, so a
+// block row holding a hub row costs its entries, not one step per block.
+// bmask must be zero on entry.
+__global__ __launch_bounds__(kTB) void k_bsr_fill_lds(const int32_t *__restrict__ rp,
+                                                      const int32_t *__restrict__ col,
+                                                      const float *__restrict__ val, int64_t R, int b,
+                                                      int64_t nbr, int64_t nw,
+                                                      const int32_t *__restrict__ bptr,
+                                                      int32_t *__restrict__ bcol,
+                                                      float *__restrict__ bval,
+                                                      unsigned long long *__restrict__ bmask)
+{
+    extern __shared__ uint32_t sm[];
+    uint32_t *bmp = sm;                                   // nw words
+    int32_t *pre = reinterpret_cast<int32_t *>(sm + nw);  // nw prefix counts
+    __shared__ int32_t lrp[65];                           // the block row's row pointers (b <= 64)
+    __shared__ int tmp[kTB / kWave];
+    __shared__ int carry;
+    const int64_t bb = (int64_t)b * b;
+    for (int64_t br = blockIdx.x; br < nbr; br += gridDim.x) {
+        const int64_t r0 = br * b;
+        const int nr = (int)(R - r0 < b ? R - r0 : b);
+        for (int64_t w = threadIdx.x; w < nw; w += kTB) bmp[w] = 0u;
+        if (threadIdx.x <= nr) lrp[threadIdx.x] = rp[r0 + threadIdx.x];
+        if (threadIdx.x == 0) carry = 0;
+        __syncthreads();
+        const int64_t k0 = lrp[0], k1 = lrp[nr];
+        for (int64_t k = k0 + threadIdx.x; k < k1; k += kTB) {
+            const uint32_t c = (uint32_t)(col[k] / b);
+            atomicOr(&bmp[c >> 5], 1u << (c & 31));
+        }
+        __syncthreads();
+        for (int64_t w0 = 0; w0 < nw; w0 += kTB) {
+            const int64_t w = w0 + threadIdx.x;
+            const int pc = w < nw ? __popc(bmp[w]) : 0;
+            const int ex = block_exclusive_scan<kTB>(pc, tmp);
+            const int base = carry;
+            if (w < nw) pre[w] = base + ex;
+            __syncthreads();
+            if (threadIdx.x == kTB - 1) carry = base + ex + pc;
+            __syncthreads();
+        }
+        const int64_t blk0 = bptr[br];
+        for (int64_t w = threadIdx.x; w < nw; w += kTB) {
+            uint32_t x = bmp[w];
+            int64_t n = blk0 + pre[w];
+            while (x) {
+                bcol[n++] = (int32_t)(w * 32 + __ffs(x) - 1);
+                x &= x - 1;
+            }
+        }
+        for (int64_t k = k0 + threadIdx.x; k < k1; k += kTB) {
+            int lo = 0, hi = nr - 1;  // row of entry k: last li with lrp[li] <= k
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (lrp[mid] <= k)
+                    lo = mid;
+                else
+                    hi = mid - 1;
+            }
+            const int c = col[k];
+            const uint32_t bc = (uint32_t)(c / b);
+            const int64_t blk = blk0 + pre[bc >> 5] + __popc(bmp[bc >> 5] & ((1u << (bc & 31)) - 1u));
+            const int cc = c - (int)bc * b;
+            bval[blk * bb + (int64_t)lo * b + cc] = val[k];
+            atomicOr(&bmask[blk], 1ull << cc);
+        }
+        __syncthreads();  // before the next block row reuses the LDS
+    }
+}
+
 __global__ __launch_bounds__(kTB) void k_bsr_fill(const int32_t *__restrict__ rp,
                                                   const int32_t *__restrict__ col,
                                                   const float *__restrict__ val, int64_t R, int b,
@@ -518,7 +616,8 @@ __global__ __launch_bounds__(kTB) void k_expand_rows(const int32_t *__restrict__
 
 
 // Distinct (row/b, col/b) blocks per block row into cnt[0..nbr).  The LDS
-// bitmap kernel needs nbc/8 bytes of LDS; wider matrices use the merge.
+// bitmap kernel needs nbc/8 bytes of LDS; wider matrices use the merge (the
+// BSR fill makes the same choice).
 void launch_block_count(const int32_t *rp, const int32_t *col, int64_t R, int64_t C, int b,
                         int64_t nbr, int32_t *cnt, hipStream_t s)
 {
@@ -583,7 +682,6 @@ void radix_sort_pairs(uint64_t *ka, uint64_t *kb, uint32_t *pa, uint32_t *pb, in
             pout = (pin == nullptr) ? pspare : pin;
             pin = used;
         }
-        GS_HIP(hipStreamSynchronize(s));  // before hist is freed
     }
     *keys = kin;
     *perm = pin;
@@ -616,7 +714,6 @@ void sort_triplets(const int32_t *major, const int32_t *minor, const float *val,
     k_unpack_sorted<<<elem_grid(Z), kTB, 0, s>>>(keys, perm, val, Z, omajor, ominor, oval,
                                                  flags.as<int>());
     GS_LAUNCH_CHECK();
-    GS_HIP(hipStreamSynchronize(s));  // before the sort buffers are freed
 }
 
 void canonicalize(const gs_coo &A, bool assume_canonical, hipStream_t s, CanonCOO &out)
@@ -688,7 +785,6 @@ gs_matrix_ *csr_from_canon(CanonCOO &&c, hipStream_t s, bool plan)
         m->col = std::move(c.col);
         m->val = std::move(c.val);
         m->device_bytes = (uint64_t)(c.R + 1) * 4 + (uint64_t)c.Z * 8;
-        GS_HIP(hipStreamSynchronize(s));  // c.row is released by the caller
         if (plan) plan_csr(*m, s);
     } catch (...) {
         delete m;
@@ -714,19 +810,32 @@ uint64_t format_bytes(int fmt, int64_t R, int64_t C, int64_t Z, int64_t K, int64
     return 0;
 }
 
-int64_t count_blocks(const gs_matrix_ &csr, int b, hipStream_t s)
+void count_blocks_async(const gs_matrix_ &csr, int b, unsigned long long *total, hipStream_t s)
 {
     const int64_t nbr = ceil_div(csr.R, b);
-    if (nbr == 0 || csr.Z == 0) return 0;
+    if (nbr == 0 || csr.Z == 0) return;
     DevBuf cnt;
-    cnt.alloc((size_t)(nbr + 1) * 4, s);
+    cnt.alloc((size_t)nbr * 4, s);
     launch_block_count(csr.row_ptr.as<int32_t>(), csr.col.as<int32_t>(), csr.R, csr.C, b, nbr,
                        cnt.as<int32_t>(), s);
-    exclusive_scan_i32(cnt.as<int32_t>(), cnt.as<int32_t>(), nbr, true, s);
-    int32_t nb = 0;
-    GS_HIP(hipMemcpyAsync(&nb, cnt.as<int32_t>() + nbr, 4, hipMemcpyDeviceToHost, s));
+    const unsigned G = reduce_grid(nbr);
+    DevBuf part;
+    if (G > 1) part.alloc(sizeof(unsigned long long) * G, s);
+    k_sum_counts<<<G, kTB, 0, s>>>(cnt.as<int32_t>(), nbr, part.as<unsigned long long>(), total);
+    GS_LAUNCH_CHECK();
+    if (G > 1) add_partials_u64(part.as<unsigned long long>(), G, total, s);
+}
+
+int64_t count_blocks(const gs_matrix_ &csr, int b, hipStream_t s)
+{
+    DevBuf d;
+    d.alloc(sizeof(unsigned long long), s);
+    GS_HIP(hipMemsetAsync(d.p, 0, sizeof(unsigned long long), s));
+    count_blocks_async(csr, b, d.as<unsigned long long>(), s);
+    unsigned long long nb = 0;
+    GS_HIP(hipMemcpyAsync(&nb, d.p, sizeof nb, hipMemcpyDeviceToHost, s));
     GS_HIP(hipStreamSynchronize(s));
-    return nb;
+    return (int64_t)nb;
 }
 
 gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint64_t max_bytes,
@@ -776,7 +885,6 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
             }
             k_row_ptr<<<elem_grid(Z + 1), kTB, 0, s>>>(cols.as<int32_t>(), Z, C, m->row_ptr.as<int32_t>());
             GS_LAUNCH_CHECK();
-            GS_HIP(hipStreamSynchronize(s));  // before rows / cols are freed
             m->device_bytes = need;
             break;
         }
@@ -858,7 +966,6 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
                                                         bm.as<uint32_t>(), wpos.as<int32_t>(),
                                                         m->dia.as<float>());
                 GS_LAUNCH_CHECK();
-                GS_HIP(hipStreamSynchronize(s));  // before bm / wpos / row are freed
             }
             m->device_bytes = need;
             break;
@@ -887,17 +994,31 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
             m->bval.alloc((size_t)nb * b * b * 4, s);
             if (nb) {
                 GS_HIP(hipMemsetAsync(m->bval.p, 0, (size_t)nb * b * b * 4, s));
-                k_bsr_fill<<<grid_for(nbr * kWave), kTB, 0, s>>>(
-                    rp, col, val, R, b, nbr, m->bptr.as<int32_t>(), m->bcol.as<int32_t>(),
-                    m->bval.as<float>(), m->bmask.as<uint64_t>());
+                const int64_t nw = ceil_div(ceil_div(C, b), 32);
+                const size_t lds = (size_t)nw * 8;  // bitmap + prefix counts
+                const char *force_merge = std::getenv("GS_BLOCK_COUNT_MERGE");
+                if ((int64_t)lds + 2048 <= max_lds_bytes() && !(force_merge && *force_merge == '1')) {
+                    GS_HIP(hipMemsetAsync(m->bmask.p, 0, (size_t)nb * 8, s));
+                    k_bsr_fill_lds<<<(unsigned)std::min<int64_t>(nbr, 256 * 8), kTB, lds, s>>>(
+                        rp, col, val, R, b, nbr, nw, m->bptr.as<int32_t>(), m->bcol.as<int32_t>(),
+                        m->bval.as<float>(), m->bmask.as<unsigned long long>());
+                } else {
+                    k_bsr_fill<<<grid_for(nbr * kWave), kTB, 0, s>>>(
+                        rp, col, val, R, b, nbr, m->bptr.as<int32_t>(), m->bcol.as<int32_t>(),
+                        m->bval.as<float>(), m->bmask.as<uint64_t>());
+                }
                 GS_LAUNCH_CHECK();
                 // dense-block count (kernel choice at SpMM time)
                 DevBuf dn;
                 dn.alloc(sizeof(unsigned long long), s);
                 GS_HIP(hipMemsetAsync(dn.p, 0, sizeof(unsigned long long), s));
-                k_count_dense<<<(unsigned)std::min<int64_t>(1024, ceil_div(nb, (int64_t)kTB)), kTB, 0, s>>>(
-                    m->bmask.as<uint64_t>(), nb, kBsrDenseCols, dn.as<unsigned long long>());
+                const unsigned G = reduce_grid(nb);
+                DevBuf part;
+                if (G > 1) part.alloc(sizeof(unsigned long long) * G, s);
+                k_count_dense<<<G, kTB, 0, s>>>(m->bmask.as<uint64_t>(), nb, kBsrDenseCols,
+                                                part.as<unsigned long long>(), dn.as<unsigned long long>());
                 GS_LAUNCH_CHECK();
+                if (G > 1) add_partials_u64(part.as<unsigned long long>(), G, dn.as<unsigned long long>(), s);
                 unsigned long long dense = 0;
                 GS_HIP(hipMemcpyAsync(&dense, dn.p, sizeof dense, hipMemcpyDeviceToHost, s));
                 GS_HIP(hipStreamSynchronize(s));
@@ -973,7 +1094,6 @@ void to_coo(const gs_matrix_ &m, int32_t *row, int32_t *col, float *val, hipStre
     default: fail(GS_ERR_INVALID_ARG, "corrupt matrix handle");
     }
     GS_LAUNCH_CHECK();
-    GS_HIP(hipStreamSynchronize(s));  // before pos is freed
 }
 
 gs_matrix_ *csr_from_any(const gs_matrix_ &m, hipStream_t s)

@@ -58,6 +58,63 @@ __device__ __forceinline__ int wave_sum_i32(int v)
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
+// Workgroup-wide reductions over NT threads (a multiple of the wave width):
+// every thread passes its value and receives the workgroup's result.  tmp
+// holds NT / kWave values in LDS; the call ends with a barrier, so the next
+// call may reuse tmp.
+template <int NT>
+__device__ __forceinline__ unsigned long long block_sum_u64(unsigned long long v, unsigned long long *tmp)
+{
+    v = wave_sum_u64(v);
+    if (lane_id() == 0) tmp[threadIdx.x / kWave] = v;
+    __syncthreads();
+    unsigned long long t = 0;
+    for (int w = 0; w < NT / kWave; w++) t += tmp[w];
+    __syncthreads();
+    return t;
+}
+
+template <int NT> __device__ __forceinline__ int block_max_i32(int v, int *tmp)
+{
+    v = wave_max_i32(v);
+    if (lane_id() == 0) tmp[threadIdx.x / kWave] = v;
+    __syncthreads();
+    int t = tmp[0];
+    for (int w = 1; w < NT / kWave; w++) t = tmp[w] > t ? tmp[w] : t;
+    __syncthreads();
+    return t;
+}
+
+template <int NT> __device__ __forceinline__ int block_min_i32(int v, int *tmp)
+{
+    v = wave_min_i32(v);
+    if (lane_id() == 0) tmp[threadIdx.x / kWave] = v;
+    __syncthreads();
+    int t = tmp[0];
+    for (int w = 1; w < NT / kWave; w++) t = tmp[w] < t ? tmp[w] : t;
+    __syncthreads();
+    return t;
+}
+
+// Exclusive prefix sum of one value per thread over the workgroup (NT
+// threads); tmp holds NT / kWave ints.  Ends with a barrier.
+template <int NT> __device__ __forceinline__ int block_exclusive_scan(int x, int *tmp)
+{
+    const int lane = lane_id(), w = threadIdx.x / kWave;
+    int inc = x;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(inc, o, kWave);
+        if (lane >= o) inc += y;
+    }
+    if (lane == kWave - 1) tmp[w] = inc;
+    __syncthreads();
+    int off = 0;
+    for (int v = 0; v < w; v++) off += tmp[v];
+    __syncthreads();
+    return off + inc - x;
+}
+
 // fp32 vector of VEC elements with the alignment of its size.
 template <int VEC> struct Vec;
 template <> struct Vec<1> {

@@ -40,91 +40,152 @@ __global__ __launch_bounds__(kTB) void k_col_hist(const int32_t *__restrict__ co
 }
 
 // Column counts without global atomics (large matrices): the column indices
-// are first bucketed by their high bits (windows of W = 2^shift columns, so a
-// window's counters fit in one workgroup's LDS), then every slice of a bucket
-// is counted by one workgroup in LDS and written out whole, and the slices'
-// counts are added per column.  Four passes over the indices in all.
-constexpr int kBucketTile = kTB * 16;  // indices per tile of the bucketing passes
+// are first grouped by their high bits (buckets of 2^shift columns, so a
+// bucket's counters fit in one workgroup's LDS), then every slice of a
+// bucket is counted by one workgroup in LDS and written out whole, and the
+// slices' counts are added per column.
+constexpr int kBucketTile = kTB * 16;  // keys per tile of the bucketing passes
+constexpr int kBucketPer = kBucketTile / kTB;
 
-__global__ __launch_bounds__(kTB) void k_bucket_hist(const int32_t *__restrict__ col, int64_t Z,
+// hist[b * ntiles + t] = number of keys of tile t in bucket b.
+__global__ __launch_bounds__(kTB) void k_bucket_hist(const uint32_t *__restrict__ keys, int64_t Z,
                                                      int shift, int nb, int64_t ntiles,
                                                      int32_t *__restrict__ hist)
 {
-    __shared__ int h[256];
+    __shared__ int h[kTB];
     h[threadIdx.x] = 0;
     __syncthreads();
     const int64_t base = (int64_t)blockIdx.x * kBucketTile;
-    for (int i = 0; i < kBucketTile / kTB; i++) {
+    uint32_t v[kBucketPer];
+#pragma unroll
+    for (int i = 0; i < kBucketPer; i++) {  // all loads in flight before the counting
         const int64_t k = base + (int64_t)i * kTB + threadIdx.x;
-        if (k < Z) atomicAdd(&h[col[k] >> shift], 1);
+        v[i] = k < Z ? keys[k] : ~0u;
     }
+#pragma unroll
+    for (int i = 0; i < kBucketPer; i++)
+        if (v[i] != ~0u) atomicAdd(&h[v[i] >> shift], 1);
     __syncthreads();
     if (threadIdx.x < nb) hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
 }
 
-__global__ __launch_bounds__(kTB) void k_bucket_scatter(const int32_t *__restrict__ col, int64_t Z,
+// Writes tile t's keys of bucket b from position off[b * ntiles + t] on.
+// The tile is first grouped by bucket in LDS, so every bucket's keys leave
+// as one contiguous run (order inside a bucket is free).
+__global__ __launch_bounds__(kTB) void k_bucket_scatter(const uint32_t *__restrict__ keys, int64_t Z,
                                                         int shift, int nb, int64_t ntiles,
                                                         const int32_t *__restrict__ off,
-                                                        int32_t *__restrict__ out)
+                                                        uint32_t *__restrict__ out)
 {
-    __shared__ int run[256];
-    if (threadIdx.x < nb) run[threadIdx.x] = off[(int64_t)threadIdx.x * ntiles + blockIdx.x];
+    __shared__ int cnt[kTB], lstart[kTB], gbase[kTB], tmp[kTB / kWave];
+    __shared__ uint32_t stage[kBucketTile];
+    cnt[threadIdx.x] = 0;
+    if (threadIdx.x < nb) gbase[threadIdx.x] = off[(int64_t)threadIdx.x * ntiles + blockIdx.x];
     __syncthreads();
     const int64_t base = (int64_t)blockIdx.x * kBucketTile;
-    for (int i = 0; i < kBucketTile / kTB; i++) {
+    uint32_t v[kBucketPer];
+    int rank[kBucketPer];
+#pragma unroll
+    for (int i = 0; i < kBucketPer; i++) {
         const int64_t k = base + (int64_t)i * kTB + threadIdx.x;
-        if (k < Z) {
-            const int c = col[k];
-            out[atomicAdd(&run[c >> shift], 1)] = c;  // order inside a bucket is free
-        }
+        v[i] = k < Z ? keys[k] : ~0u;
+    }
+#pragma unroll
+    for (int i = 0; i < kBucketPer; i++) rank[i] = v[i] != ~0u ? atomicAdd(&cnt[v[i] >> shift], 1) : 0;
+    __syncthreads();
+    lstart[threadIdx.x] = block_exclusive_scan<kTB>(cnt[threadIdx.x], tmp);
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kBucketPer; i++)
+        if (v[i] != ~0u) stage[lstart[v[i] >> shift] + rank[i]] = v[i];
+    __syncthreads();
+    const int n = (int)(Z - base < kBucketTile ? Z - base : kBucketTile);
+    for (int j = threadIdx.x; j < n; j += kTB) {
+        const uint32_t x = stage[j];
+        const int bk = (int)(x >> shift);
+        out[gbase[bk] + (j - lstart[bk])] = x;
     }
 }
 
-// Block (b, s): slice s of bucket b's indices, counted into W LDS counters.
-__global__ __launch_bounds__(kTB) void k_bucket_count(const int32_t *__restrict__ cols,
+// Workgroup (b, sl): slice sl of bucket b's keys, counted into 2^shift LDS
+// counters and written out whole to partial[(b * slices + sl) << shift ..].
+// 128 KiB of LDS allows one workgroup per CU, so it has 16 waves to keep
+// enough key loads in flight.
+constexpr int kCountTB = 1024;
+
+__global__ __launch_bounds__(kCountTB) void k_bucket_count(const uint32_t *__restrict__ keys,
                                                       const int32_t *__restrict__ off, int64_t ntiles,
                                                       int shift, int slices,
-                                                      int32_t *__restrict__ partial)
+                                                      uint32_t *__restrict__ partial)
 {
-    extern __shared__ int cnt[];
-    const int W = 1 << shift;
+    extern __shared__ uint32_t lw[];
+    const int words = 1 << shift;
     const int b = blockIdx.x / slices, sl = blockIdx.x % slices;
-    for (int j = threadIdx.x; j < W; j += kTB) cnt[j] = 0;
+    for (int j = threadIdx.x; j < words; j += kCountTB) lw[j] = 0;
     __syncthreads();
     const int64_t b0 = off[(int64_t)b * ntiles], b1 = off[(int64_t)(b + 1) * ntiles];
     const int64_t per = (b1 - b0 + slices - 1) / slices;
     const int64_t k0 = b0 + sl * per, k1 = k0 + per < b1 ? k0 + per : b1;
-    const int cbase = b << shift;
-    for (int64_t k = k0 + threadIdx.x; k < k1; k += kTB) atomicAdd(&cnt[cols[k] - cbase], 1);
+    const uint32_t kbase = (uint32_t)b << shift;
+    constexpr int U = 8;  // key loads in flight per thread
+    for (int64_t kb = k0 + threadIdx.x; kb < k1; kb += U * kCountTB) {
+        uint32_t v[U];
+#pragma unroll
+        for (int u = 0; u < U; u++) v[u] = kb + u * kCountTB < k1 ? keys[kb + u * kCountTB] - kbase : ~0u;
+#pragma unroll
+        for (int u = 0; u < U; u++)
+            if (v[u] != ~0u) atomicAdd(&lw[v[u]], 1u);
+    }
     __syncthreads();
-    int32_t *out = partial + (int64_t)blockIdx.x * W;
-    for (int j = threadIdx.x; j < W; j += kTB) out[j] = cnt[j];
+    uint32_t *out = partial + (int64_t)blockIdx.x * words;
+    for (int j = threadIdx.x; j < words; j += kCountTB) out[j] = lw[j];
 }
 
-__global__ __launch_bounds__(kTB) void k_bucket_reduce(const int32_t *__restrict__ partial, int64_t C,
-                                                       int shift, int slices,
-                                                       int32_t *__restrict__ cc)
+// out[c] for c < n: the sum of counter c over the slices.
+__global__ __launch_bounds__(kTB) void k_bucket_reduce(const uint32_t *__restrict__ partial, int64_t n,
+                                                       int shift, int slices, uint32_t *__restrict__ out)
 {
     const int64_t W = 1ll << shift;
-    for (int64_t c = (int64_t)blockIdx.x * kTB + threadIdx.x; c < C; c += (int64_t)gridDim.x * kTB) {
+    for (int64_t c = (int64_t)blockIdx.x * kTB + threadIdx.x; c < n; c += (int64_t)gridDim.x * kTB) {
         const int64_t b = c >> shift, j = c & (W - 1);
-        int sum = 0;
-        for (int s = 0; s < slices; s++) sum += partial[(b * slices + s) * W + j];
-        cc[c] = sum;
+        uint32_t acc = 0;
+        for (int s = 0; s < slices; s++) acc += partial[(b * slices + s) * W + j];
+        out[c] = acc;
     }
 }
 
-// Statistics of a count sequence cnt[i] = (ptr ? ptr[i+1]-ptr[i] : vals[i]).
-// Each workgroup reduces in registers, then across its waves in LDS, and
-// issues one set of atomics (the grid is kept small, so the few atomics on
-// the shared accumulator do not queue up).
+// Statistics of a count sequence cnt[i] = (ptr ? ptr[i+1]-ptr[i] : vals[i]):
+// sum of squares, sum of adjacent absolute differences, max, min.  Each
+// workgroup reduces its share and writes one partial record; a one-workgroup
+// grid writes the final fields of *acc itself, otherwise k_stats_final
+// combines the partials (many atomics on one record would queue up).
+struct StatPart {
+    unsigned long long s2, bn;
+    int mx, mn;
+};
+
+__device__ __forceinline__ void store_stats(FeatAcc *acc, int is_row, const StatPart &p)
+{
+    if (is_row) {
+        acc->s2r = p.s2;
+        acc->bnr = p.bn;
+        acc->maxr = p.mx;
+        acc->minr = p.mn;
+    } else {
+        acc->s2c = p.s2;
+        acc->bnc = p.bn;
+        acc->maxc = p.mx;
+        acc->minc = p.mn;
+    }
+}
+
 __global__ __launch_bounds__(kTB) void k_count_stats(const int32_t *__restrict__ ptr,
                                                      const int32_t *__restrict__ vals, int64_t n,
-                                                     int is_row, FeatAcc *__restrict__ acc)
+                                                     int is_row, FeatAcc *__restrict__ acc,
+                                                     StatPart *__restrict__ part)
 {
-    constexpr int NWV = kTB / kWave;
-    __shared__ unsigned long long s_s2[NWV], s_bn[NWV];
-    __shared__ int s_mx[NWV], s_mn[NWV];
+    __shared__ unsigned long long t64[kTB / kWave];
+    __shared__ int t32[kTB / kWave];
     unsigned long long s2 = 0, bn = 0;
     int mx = 0, mn = INT_MAX;
     for (int64_t i = (int64_t)blockIdx.x * kTB + threadIdx.x; i < n;
@@ -138,42 +199,58 @@ __global__ __launch_bounds__(kTB) void k_count_stats(const int32_t *__restrict__
             bn += (unsigned long long)(c1 > c ? c1 - c : c - c1);
         }
     }
-    s2 = wave_sum_u64(s2);
-    bn = wave_sum_u64(bn);
-    mx = wave_max_i32(mx);
-    mn = wave_min_i32(mn);
-    const int w = threadIdx.x / kWave;
-    if (lane_id() == 0) {
-        s_s2[w] = s2;
-        s_bn[w] = bn;
-        s_mx[w] = mx;
-        s_mn[w] = mn;
-    }
-    __syncthreads();
+    StatPart p;
+    p.s2 = block_sum_u64<kTB>(s2, t64);
+    p.bn = block_sum_u64<kTB>(bn, t64);
+    p.mx = block_max_i32<kTB>(mx, t32);
+    p.mn = block_min_i32<kTB>(mn, t32);
     if (threadIdx.x != 0) return;
-    for (int v = 1; v < NWV; v++) {
-        s2 += s_s2[v];
-        bn += s_bn[v];
-        mx = s_mx[v] > mx ? s_mx[v] : mx;
-        mn = s_mn[v] < mn ? s_mn[v] : mn;
+    if (gridDim.x == 1)
+        store_stats(acc, is_row, p);
+    else
+        part[blockIdx.x] = p;
+}
+
+__global__ __launch_bounds__(kTB) void k_stats_final(const StatPart *__restrict__ part, int64_t G,
+                                                     int is_row, FeatAcc *__restrict__ acc)
+{
+    __shared__ unsigned long long t64[kTB / kWave];
+    __shared__ int t32[kTB / kWave];
+    unsigned long long s2 = 0, bn = 0;
+    int mx = 0, mn = INT_MAX;
+    for (int64_t g = threadIdx.x; g < G; g += kTB) {
+        const StatPart q = part[g];
+        s2 += q.s2;
+        bn += q.bn;
+        mx = q.mx > mx ? q.mx : mx;
+        mn = q.mn < mn ? q.mn : mn;
     }
-    if (is_row) {
-        atomicAdd(&acc->s2r, s2);
-        atomicAdd(&acc->bnr, bn);
-        atomicMax(&acc->maxr, mx);
-        atomicMin(&acc->minr, mn);
-    } else {
-        atomicAdd(&acc->s2c, s2);
-        atomicAdd(&acc->bnc, bn);
-        atomicMax(&acc->maxc, mx);
-        atomicMin(&acc->minc, mn);
-    }
+    StatPart p;
+    p.s2 = block_sum_u64<kTB>(s2, t64);
+    p.bn = block_sum_u64<kTB>(bn, t64);
+    p.mx = block_max_i32<kTB>(mx, t32);
+    p.mn = block_min_i32<kTB>(mn, t32);
+    if (threadIdx.x == 0) store_stats(acc, is_row, p);
 }
 
 inline unsigned stats_grid(int64_t n)
 {
-    int64_t g = ceil_div(n, (int64_t)kTB * 8);
-    return (unsigned)(g < 1 ? 1 : g > 512 ? 512 : g);
+    int64_t g = ceil_div(n, (int64_t)kTB * 4);
+    return (unsigned)(g < 1 ? 1 : g > 2048 ? 2048 : g);
+}
+
+// Statistics of n counts into the row (is_row) or column fields of *acc.
+void count_stats(const int32_t *ptr, const int32_t *vals, int64_t n, int is_row, FeatAcc *acc, hipStream_t s)
+{
+    const unsigned G = stats_grid(n);
+    DevBuf part;
+    if (G > 1) part.alloc(sizeof(StatPart) * G, s);
+    k_count_stats<<<G, kTB, 0, s>>>(ptr, vals, n, is_row, acc, part.as<StatPart>());
+    GS_HIP(hipGetLastError());
+    if (G > 1) {
+        k_stats_final<<<1, kTB, 0, s>>>(part.as<StatPart>(), G, is_row, acc);
+        GS_HIP(hipGetLastError());
+    }
 }
 
 // Diagonal occupancy bitmap: bit (col - row + R - 1) is set for every entry.
@@ -185,13 +262,14 @@ inline unsigned stats_grid(int64_t n)
 // bitmap out whole; k_diag_or then ORs the per-workgroup bitmaps word by
 // word.  No global atomics.
 //
-// Large spans: one wavefront per row marks the global bitmap with atomicOr,
+// Large spans: one wavefront per row marks a global bitmap with atomicOr,
 // skipping the atomic when the bit is already set (bits only ever get set,
 // and the main diagonal alone gets one hit per row).
 constexpr int64_t kDiagLdsRows = 2048;    // rows per workgroup (8 KiB row_ptr slice)
 constexpr int kDiagParts = 256;           // workgroups (partial bitmaps)
+constexpr int kDiagTB = 1024;             // 16 waves per workgroup hide the gather latency
 
-__global__ __launch_bounds__(kTB) void k_diag_lds(const int32_t *__restrict__ rp,
+__global__ __launch_bounds__(kDiagTB) void k_diag_lds(const int32_t *__restrict__ rp,
                                                   const int32_t *__restrict__ col, int64_t R,
                                                   int64_t nw, int64_t rows_per,
                                                   uint32_t *__restrict__ partial)
@@ -202,18 +280,18 @@ __global__ __launch_bounds__(kTB) void k_diag_lds(const int32_t *__restrict__ rp
     const int64_t r0 = (int64_t)blockIdx.x * rows_per < R ? (int64_t)blockIdx.x * rows_per : R;
     const int64_t r1 = r0 + rows_per < R ? r0 + rows_per : R;
     const int nr = (int)(r1 - r0);
-    for (int64_t w = threadIdx.x; w < nw; w += kTB) lbm[w] = 0;
-    for (int i = threadIdx.x; i <= nr; i += kTB) lrp[i] = rp[r0 + i];
+    for (int64_t w = threadIdx.x; w < nw; w += kDiagTB) lbm[w] = 0;
+    for (int i = threadIdx.x; i <= nr; i += kDiagTB) lrp[i] = rp[r0 + i];
     __syncthreads();
     const int64_t k0 = lrp[0], k1 = lrp[nr];
     constexpr int U = 4;  // column loads in flight per thread
-    for (int64_t kb = k0 + threadIdx.x; kb < k1; kb += U * kTB) {
+    for (int64_t kb = k0 + threadIdx.x; kb < k1; kb += U * kDiagTB) {
         int c[U];
 #pragma unroll
-        for (int u = 0; u < U; u++) c[u] = kb + u * kTB < k1 ? col[kb + u * kTB] : 0;
+        for (int u = 0; u < U; u++) c[u] = kb + u * kDiagTB < k1 ? col[kb + u * kDiagTB] : 0;
 #pragma unroll
         for (int u = 0; u < U; u++) {
-            const int64_t k = kb + u * kTB;
+            const int64_t k = kb + u * kDiagTB;
             if (k >= k1) break;
             // last row i of the range with lrp[i] <= k (empty rows share their start)
             int lo = 0, hi = nr - 1;
@@ -231,7 +309,7 @@ __global__ __launch_bounds__(kTB) void k_diag_lds(const int32_t *__restrict__ rp
     }
     __syncthreads();
     uint32_t *out = partial + (int64_t)blockIdx.x * nw;
-    for (int64_t w = threadIdx.x; w < nw; w += kTB) out[w] = lbm[w];
+    for (int64_t w = threadIdx.x; w < nw; w += kDiagTB) out[w] = lbm[w];
 }
 
 // Block of 1024 threads = 64 words x 16 slices of the partial bitmaps.
@@ -258,27 +336,49 @@ __global__ __launch_bounds__(kTB) void k_mark_diags(const int32_t *__restrict__ 
 {
     const int lane = lane_id();
     const int64_t waves = (int64_t)gridDim.x * (kTB / kWave);
+    constexpr int U = 8;  // entries in flight per lane (a hub row is one wave's work)
     for (int64_t i = ((int64_t)blockIdx.x * kTB + threadIdx.x) / kWave; i < R; i += waves) {
-        for (int64_t k = rp[i] + lane; k < rp[i + 1]; k += kWave) {
-            int64_t sidx = (int64_t)col[k] - i + R - 1;
-            const uint32_t bit = 1u << (sidx & 31);
-            // the check may read a stale copy cached near this workgroup:
-            // then the (idempotent) atomic is simply issued
-            if (!(__hip_atomic_load(&bm[sidx >> 5], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) & bit))
-                atomicOr(&bm[sidx >> 5], bit);
+        const int64_t e = rp[i + 1];
+        for (int64_t kb = rp[i] + lane; kb < e; kb += U * kWave) {
+            int64_t sidx[U];
+#pragma unroll
+            for (int u = 0; u < U; u++)
+                sidx[u] = kb + u * kWave < e ? (int64_t)col[kb + u * kWave] - i + R - 1 : -1;
+            uint32_t seen[U];
+#pragma unroll
+            for (int u = 0; u < U; u++)
+                // the check may read a stale copy cached near this workgroup:
+                // then the (idempotent) atomic is simply issued
+                seen[u] = sidx[u] < 0 ? ~0u
+                                      : __hip_atomic_load(&bm[sidx[u] >> 5], __ATOMIC_RELAXED,
+                                                          __HIP_MEMORY_SCOPE_WORKGROUP);
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                if (sidx[u] < 0) continue;
+                const uint32_t bit = 1u << (sidx[u] & 31);
+                if (!(seen[u] & bit)) atomicOr(&bm[sidx[u] >> 5], bit);
+            }
         }
     }
 }
 
+// Population count of the bitmap: one partial per workgroup (or the total
+// itself, added to *total, from a one-workgroup grid).
 __global__ __launch_bounds__(kTB) void k_popc_total(const uint32_t *__restrict__ bm, int64_t nw,
+                                                    unsigned long long *__restrict__ part,
                                                     unsigned long long *__restrict__ total)
 {
+    __shared__ unsigned long long t64[kTB / kWave];
     unsigned long long s = 0;
     for (int64_t w = (int64_t)blockIdx.x * kTB + threadIdx.x; w < nw;
          w += (int64_t)gridDim.x * kTB)
         s += __popc(bm[w]);
-    s = wave_sum_u64(s);
-    if (lane_id() == 0 && s) atomicAdd(total, s);
+    s = block_sum_u64<kTB>(s, t64);
+    if (threadIdx.x != 0) return;
+    if (gridDim.x == 1)
+        *total += s;
+    else
+        part[blockIdx.x] = s;
 }
 
 // R*S2 - Z^2 >= 0 (Cauchy-Schwarz), formed exactly in 128-bit arithmetic.
@@ -289,6 +389,19 @@ double population_dev(int64_t n, int64_t Z, uint64_t s2)
                             (unsigned __int128)(uint64_t)Z * (uint64_t)Z;
     double q = (double)num / ((double)n * (double)n);
     return std::sqrt(q);
+}
+
+}  // namespace
+
+namespace {
+
+// Column-count buckets of 2^shift columns: 32768 counters (128 KiB of LDS),
+// fewer where LDS is smaller.
+int bucket_shift()
+{
+    int w = 15;
+    while (w > 10 && ((int64_t)4 << w) > max_lds_bytes()) w--;
+    return w;
 }
 
 }  // namespace
@@ -305,11 +418,10 @@ void diag_bitmap(const int32_t *rp, const int32_t *col, int64_t R, int64_t C, in
         DevBuf part;
         part.alloc((size_t)(P * nw) * 4, s);
         const size_t lds = (size_t)(nw + rows_per + 1) * 4;
-        k_diag_lds<<<(unsigned)P, kTB, lds, s>>>(rp, col, R, nw, rows_per, part.as<uint32_t>());
+        k_diag_lds<<<(unsigned)P, kDiagTB, lds, s>>>(rp, col, R, nw, rows_per, part.as<uint32_t>());
         GS_HIP(hipGetLastError());
         k_diag_or<<<(unsigned)ceil_div(nw, 64), 1024, 0, s>>>(part.as<uint32_t>(), P, nw, bm);
         GS_HIP(hipGetLastError());
-        GS_HIP(hipStreamSynchronize(s));  // before part is freed
         return;
     }
     GS_HIP(hipMemsetAsync(bm, 0, (size_t)nw * 4, s));
@@ -323,9 +435,8 @@ void diag_bitmap(const int32_t *rp, const int32_t *col, int64_t R, int64_t C, in
 // matrix is large enough to pay for the extra passes, atomics otherwise.
 void column_counts(const int32_t *col, int64_t C, int64_t Z, int32_t *cc, hipStream_t s)
 {
-    int shift = 15;  // 32768 counters = 128 KiB of LDS
-    while (shift > 10 && ((int64_t)4 << shift) > max_lds_bytes()) shift--;
-    const int64_t nb = (C + (1ll << shift) - 1) >> shift;
+    const int shift = bucket_shift();
+    const int64_t nb = ceil_div(C, 1ll << shift);
     if (Z < (1 << 20) || nb > 256 || std::getenv("GS_COLHIST_ATOMIC") != nullptr) {
         GS_HIP(hipMemsetAsync(cc, 0, (size_t)C * 4, s));
         if (Z > 0) {
@@ -334,6 +445,7 @@ void column_counts(const int32_t *col, int64_t C, int64_t Z, int32_t *cc, hipStr
         }
         return;
     }
+    const uint32_t *keys = reinterpret_cast<const uint32_t *>(col);
     const int64_t ntiles = ceil_div(Z, (int64_t)kBucketTile);
     // about 512 workgroups in all (one at a time per CU at 128 KiB of LDS)
     const int slices = (int)std::max<int64_t>(1, std::min<int64_t>(64, ceil_div(512, nb)));
@@ -341,18 +453,18 @@ void column_counts(const int32_t *col, int64_t C, int64_t Z, int32_t *cc, hipStr
     hist.alloc((size_t)(nb * ntiles + 1) * 4, s);
     sorted.alloc((size_t)Z * 4, s);
     partial.alloc(((size_t)(nb * slices) << shift) * 4, s);
-    k_bucket_hist<<<(unsigned)ntiles, kTB, 0, s>>>(col, Z, shift, (int)nb, ntiles, hist.as<int32_t>());
+    k_bucket_hist<<<(unsigned)ntiles, kTB, 0, s>>>(keys, Z, shift, (int)nb, ntiles, hist.as<int32_t>());
     GS_HIP(hipGetLastError());
     exclusive_scan_i32(hist.as<int32_t>(), hist.as<int32_t>(), nb * ntiles, true, s);
-    k_bucket_scatter<<<(unsigned)ntiles, kTB, 0, s>>>(col, Z, shift, (int)nb, ntiles, hist.as<int32_t>(),
-                                                      sorted.as<int32_t>());
+    k_bucket_scatter<<<(unsigned)ntiles, kTB, 0, s>>>(keys, Z, shift, (int)nb, ntiles, hist.as<int32_t>(),
+                                                      sorted.as<uint32_t>());
     GS_HIP(hipGetLastError());
-    k_bucket_count<<<(unsigned)(nb * slices), kTB, (size_t)4 << shift, s>>>(
-        sorted.as<int32_t>(), hist.as<int32_t>(), ntiles, shift, slices, partial.as<int32_t>());
+    k_bucket_count<<<(unsigned)(nb * slices), kCountTB, (size_t)4 << shift, s>>>(
+        sorted.as<uint32_t>(), hist.as<int32_t>(), ntiles, shift, slices, partial.as<uint32_t>());
     GS_HIP(hipGetLastError());
-    k_bucket_reduce<<<elem_grid(C), kTB, 0, s>>>(partial.as<int32_t>(), C, shift, slices, cc);
+    k_bucket_reduce<<<elem_grid(C), kTB, 0, s>>>(partial.as<uint32_t>(), C, shift, slices,
+                                                 reinterpret_cast<uint32_t *>(cc));
     GS_HIP(hipGetLastError());
-    GS_HIP(hipStreamSynchronize(s));  // before the temporaries are freed
 }
 
 void features_from_csr(const gs_matrix_ &csr, hipStream_t s, gs_features *out)
@@ -361,34 +473,40 @@ void features_from_csr(const gs_matrix_ &csr, hipStream_t s, gs_features *out)
     const int32_t *rp = csr.row_ptr.as<int32_t>();
     const int32_t *col = csr.col.as<int32_t>();
 
-    FeatAcc h = {0, 0, 0, 0, 0, INT_MAX, 0, INT_MAX};
-    unsigned long long nd = 0;
-    DevBuf acc, cc, bm, ndv;
-    acc.alloc(sizeof(FeatAcc), s);
-    ndv.alloc(sizeof(unsigned long long), s);
-    GS_HIP(hipMemcpyAsync(acc.p, &h, sizeof h, hipMemcpyHostToDevice, s));
-    GS_HIP(hipMemsetAsync(ndv.p, 0, sizeof(unsigned long long), s));
+    // every aggregate lands in one device record, read back once
+    struct Out {
+        FeatAcc acc;
+        unsigned long long nd, nb16;
+    } o = {{0, 0, 0, 0, 0, INT_MAX, 0, INT_MAX}, 0, 0};
+    DevBuf d, cc, bm;
+    d.alloc(sizeof(Out), s);
+    GS_HIP(hipMemcpyAsync(d.p, &o, sizeof o, hipMemcpyHostToDevice, s));
+    Out *dout = d.as<Out>();
     if (R > 0) {
-        k_count_stats<<<stats_grid(R), kTB, 0, s>>>(rp, nullptr, R, 1, acc.as<FeatAcc>());
-        GS_HIP(hipGetLastError());
+        count_stats(rp, nullptr, R, 1, &dout->acc, s);
     }
     if (C > 0) {
         cc.alloc((size_t)C * 4, s);
         column_counts(col, C, Z, cc.as<int32_t>(), s);
-        k_count_stats<<<stats_grid(C), kTB, 0, s>>>(nullptr, cc.as<int32_t>(), C, 0, acc.as<FeatAcc>());
-        GS_HIP(hipGetLastError());
+        count_stats(nullptr, cc.as<int32_t>(), C, 0, &dout->acc, s);
     }
     if (Z > 0) {
         const int64_t nw = ceil_div(R + C - 1, 32);
         bm.alloc((size_t)nw * 4, s);
         diag_bitmap(rp, col, R, C, Z, bm.as<uint32_t>(), s);
-        k_popc_total<<<elem_grid(nw), kTB, 0, s>>>(bm.as<uint32_t>(), nw, ndv.as<unsigned long long>());
+        const unsigned G = stats_grid(nw);
+        DevBuf part;
+        if (G > 1) part.alloc(sizeof(unsigned long long) * G, s);
+        k_popc_total<<<G, kTB, 0, s>>>(bm.as<uint32_t>(), nw, part.as<unsigned long long>(), &dout->nd);
         GS_HIP(hipGetLastError());
+        if (G > 1) add_partials_u64(part.as<unsigned long long>(), G, &dout->nd, s);
     }
-    GS_HIP(hipMemcpyAsync(&h, acc.p, sizeof h, hipMemcpyDeviceToHost, s));
-    GS_HIP(hipMemcpyAsync(&nd, ndv.p, sizeof nd, hipMemcpyDeviceToHost, s));
+    count_blocks_async(csr, 16, &dout->nb16, s);
+    GS_HIP(hipMemcpyAsync(&o, d.p, sizeof o, hipMemcpyDeviceToHost, s));
     GS_HIP(hipStreamSynchronize(s));
-    const int64_t nb16 = count_blocks(csr, 16, s);
+    const FeatAcc &h = o.acc;
+    const unsigned long long nd = o.nd;
+    const int64_t nb16 = (int64_t)o.nb16;
 
     gs_features &f = *out;
     f.n_rows = R;

@@ -161,11 +161,16 @@ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 void exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, bool out_has_total,
                         hipStream_t s);
 
+// *out += part[0] + ... + part[G-1], enqueued on s: the second level of the
+// reductions whose workgroups leave one partial each (one workgroup's atomics
+// on a shared word are cheap, thousands queue up).
+void add_partials_u64(const unsigned long long *part, int64_t G, unsigned long long *out, hipStream_t s);
+
 // Stable LSD radix sort of n 64-bit keys on the 8-bit digits at `shifts`,
 // least significant first, carrying a 32-bit payload that starts as the
 // identity (the key's input position).  Ping-pongs between (ka, pa) and
 // (kb, pb); *keys / *perm receive the buffers holding the result (*perm is
-// null when no pass ran: the identity).  Synchronises s.
+// null when no pass ran: the identity).  Enqueued on s.
 void radix_sort_pairs(uint64_t *ka, uint64_t *kb, uint32_t *pa, uint32_t *pb, int64_t n,
                       const std::vector<int> &shifts, hipStream_t s, uint64_t **keys,
                       uint32_t **perm);
@@ -202,6 +207,8 @@ uint64_t format_bytes(int fmt, int64_t R, int64_t C, int64_t Z, int64_t K, int64
 
 // Counts distinct (row/b, col/b) blocks of a CSR matrix (device, synchronises).
 int64_t count_blocks(const gs_matrix_ &csr, int b, hipStream_t s);
+// Same, added to *total [dev] without waiting for the result.
+void count_blocks_async(const gs_matrix_ &csr, int b, unsigned long long *total, hipStream_t s);
 
 // --------------------------------------------------- features (gs_features)
 

@@ -54,10 +54,14 @@ void *dev_alloc(size_t bytes, hipStream_t s)
 void dev_free(void *p, hipStream_t s)
 {
     if (!p) return;
-    if (g_alloc.free)
-        g_alloc.free(p, s, g_alloc.ctx);
-    else
+    if (g_alloc.free) {
+        g_alloc.free(p, s, g_alloc.ctx);  // stream-ordered by contract
+    } else {
+        // the library frees temporaries while work using them may still be
+        // queued on s
+        (void)hipStreamSynchronize(s);
         (void)hipFree(p);
+    }
 }
 
 void ensure_work(gs_matrix_ &m, size_t bytes, hipStream_t s)

@@ -75,6 +75,17 @@ __global__ __launch_bounds__(kSB) void k_scan_tiles(const int32_t *in, int32_t *
     }
 }
 
+// *out += part[0] + ... + part[G-1] (one workgroup).
+__global__ __launch_bounds__(kSB) void k_add_partials(const unsigned long long *__restrict__ part, int64_t G,
+                                                      unsigned long long *__restrict__ out)
+{
+    __shared__ unsigned long long t64[kSB / kWave];
+    unsigned long long t = 0;
+    for (int64_t g = threadIdx.x; g < G; g += kSB) t += part[g];
+    t = block_sum_u64<kSB>(t, t64);
+    if (threadIdx.x == 0) *out += t;
+}
+
 }  // namespace
 
 void exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, bool out_has_total,
@@ -98,9 +109,13 @@ void exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, bool out_has
     k_scan_tiles<<<(unsigned)tiles, kSB, 0, s>>>(in, out, n, sums.as<int32_t>(),
                                                   out_has_total ? 1 : 0);
     GS_HIP(hipGetLastError());
-    // sums is freed when it goes out of scope; keep it alive until the
-    // kernels that read it have run.
-    GS_HIP(hipStreamSynchronize(s));
+}
+
+void add_partials_u64(const unsigned long long *part, int64_t G, unsigned long long *out, hipStream_t s)
+{
+    if (G <= 0) return;
+    k_add_partials<<<1, kSB, 0, s>>>(part, G, out);
+    GS_HIP(hipGetLastError());
 }
 
 }  // namespace gs

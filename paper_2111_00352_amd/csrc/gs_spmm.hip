@@ -714,7 +714,6 @@ void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s)
                                                    m.empty_rows.as<int32_t>());
         GS_HIP(hipGetLastError());
     }
-    GS_HIP(hipStreamSynchronize(s));  // before the temporaries are freed
 }
 
 // --------------------------------------------------------------- launchers

@@ -210,13 +210,27 @@ struct PlanStats {
     int maxlen, n_long, n_huge;
 };
 
+// Row-length statistics: one partial record per workgroup (a one-workgroup
+// grid writes the result itself); k_plan_stats_final combines the partials.
+__device__ __forceinline__ PlanStats block_plan_stats(unsigned long long sum, unsigned long long sum2, int mx,
+                                                      int nl, int nh)
+{
+    __shared__ unsigned long long t64[kBlock / kWave];
+    __shared__ int t32[kBlock / kWave];
+    PlanStats p;
+    p.sum = block_sum_u64<kBlock>(sum, t64);
+    p.sum2 = block_sum_u64<kBlock>(sum2, t64);
+    p.maxlen = block_max_i32<kBlock>(mx, t32);
+    p.n_long = (int)block_sum_u64<kBlock>((unsigned long long)nl, t64);
+    p.n_huge = (int)block_sum_u64<kBlock>((unsigned long long)nh, t64);
+    return p;
+}
+
 __global__ __launch_bounds__(kBlock) void k_plan_stats(const int32_t *__restrict__ rp, int64_t R,
                                                        int thr, int wg_thr,
+                                                       PlanStats *__restrict__ part,
                                                        PlanStats *__restrict__ st)
 {
-    constexpr int NW = kBlock / kWave;
-    __shared__ unsigned long long s_sum[NW], s_sum2[NW];
-    __shared__ int s_max[NW], s_long[NW], s_huge[NW];
     unsigned long long sum = 0, sum2 = 0;
     int mx = 0, nl = 0, nh = 0;
     for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < R;
@@ -228,33 +242,25 @@ __global__ __launch_bounds__(kBlock) void k_plan_stats(const int32_t *__restrict
         nl += len > thr;
         nh += len > wg_thr;
     }
-    sum = wave_sum_u64(sum);
-    sum2 = wave_sum_u64(sum2);
-    mx = wave_max_i32(mx);
-    nl = wave_sum_i32(nl);
-    nh = wave_sum_i32(nh);
-    const int w = threadIdx.x / kWave;
-    if (threadIdx.x % kWave == 0) {
-        s_sum[w] = sum;
-        s_sum2[w] = sum2;
-        s_max[w] = mx;
-        s_long[w] = nl;
-        s_huge[w] = nh;
+    const PlanStats p = block_plan_stats(sum, sum2, mx, nl, nh);
+    if (threadIdx.x == 0) (gridDim.x == 1 ? *st : part[blockIdx.x]) = p;
+}
+
+__global__ __launch_bounds__(kBlock) void k_plan_stats_final(const PlanStats *__restrict__ part, int64_t G,
+                                                             PlanStats *__restrict__ st)
+{
+    unsigned long long sum = 0, sum2 = 0;
+    int mx = 0, nl = 0, nh = 0;
+    for (int64_t g = threadIdx.x; g < G; g += kBlock) {
+        const PlanStats q = part[g];
+        sum += q.sum;
+        sum2 += q.sum2;
+        mx = q.maxlen > mx ? q.maxlen : mx;
+        nl += q.n_long;
+        nh += q.n_huge;
     }
-    __syncthreads();
-    if (threadIdx.x != 0) return;
-    for (int v = 1; v < NW; v++) {
-        sum += s_sum[v];
-        sum2 += s_sum2[v];
-        mx = s_max[v] > mx ? s_max[v] : mx;
-        nl += s_long[v];
-        nh += s_huge[v];
-    }
-    atomicAdd(&st->sum, sum);
-    atomicAdd(&st->sum2, sum2);
-    atomicMax(&st->maxlen, mx);
-    atomicAdd(&st->n_long, nl);
-    atomicAdd(&st->n_huge, nh);
+    const PlanStats p = block_plan_stats(sum, sum2, mx, nl, nh);
+    if (threadIdx.x == 0) *st = p;
 }
 
 __global__ __launch_bounds__(kBlock) void k_plan_keys(const int32_t *__restrict__ rp, int64_t R,
@@ -313,6 +319,12 @@ inline unsigned plan_grid(int64_t n)
     return (unsigned)(g < 1 ? 1 : g > 4096 ? 4096 : g);
 }
 
+inline unsigned stats_grid(int64_t n)
+{
+    int64_t g = ceil_div(n, (int64_t)kBlock * 4);
+    return (unsigned)(g < 1 ? 1 : g > 2048 ? 2048 : g);
+}
+
 }  // namespace
 
 void plan_csr(gs_matrix_ &m, hipStream_t s)
@@ -327,11 +339,16 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
 
     PlanStats st = {0, 0, 0, 0, 0};
     if (R > 0) {
-        DevBuf d_st;
+        const unsigned G = stats_grid(R);
+        DevBuf d_st, part;
         d_st.alloc(sizeof st, s);
-        GS_HIP(hipMemcpyAsync(d_st.p, &st, sizeof st, hipMemcpyHostToDevice, s));
-        k_plan_stats<<<plan_grid(R), kBlock, 0, s>>>(rp, R, thr, wg_thr, d_st.as<PlanStats>());
+        if (G > 1) part.alloc(sizeof(PlanStats) * G, s);
+        k_plan_stats<<<G, kBlock, 0, s>>>(rp, R, thr, wg_thr, part.as<PlanStats>(), d_st.as<PlanStats>());
         GS_HIP(hipGetLastError());
+        if (G > 1) {
+            k_plan_stats_final<<<1, kBlock, 0, s>>>(part.as<PlanStats>(), G, d_st.as<PlanStats>());
+            GS_HIP(hipGetLastError());
+        }
         GS_HIP(hipMemcpyAsync(&st, d_st.p, sizeof st, hipMemcpyDeviceToHost, s));
         GS_HIP(hipStreamSynchronize(s));
     }
@@ -399,7 +416,6 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
     } else {
         GS_HIP(hipMemsetAsync(m.long_first.p, 0, 4, s));
     }
-    GS_HIP(hipStreamSynchronize(s));  // before the sort buffers are freed
     m.csr_planned = true;
 }
 

@@ -454,6 +454,13 @@ def test_diagonal_bitmap_paths_agree(monkeypatch, path):
         check_layout(case, "dia")
 
 
+def test_wide_diagonal_bitmap():
+    # a span of 1.6 million diagonals and 700,001 rows is too wide for the
+    # per-workgroup LDS bitmap, so the global-atomic path runs by itself,
+    # with each wave's batches of entries in flight
+    check_features(_random_case(700_001, 900_000, 1_100_000, 96, empty=0.1))
+
+
 @pytest.mark.parametrize("path", ["bucketed", "atomic"])
 def test_column_count_paths_agree(monkeypatch, path):
     # bucketed LDS counting (over a million entries, several 32k-column
