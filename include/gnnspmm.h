@@ -82,7 +82,7 @@ typedef struct {
 } gs_build_opts;
 
 /* Optional device allocator (e.g. PyTorch's caching allocator).  alloc must
- * return memory usable on the given stream, or NULL.  The hooks must be
+ * return memory usable on the given stream, aligned to 256 bytes, or NULL.  The hooks must be
  * stream-ordered: free(p, s) can be called while work already enqueued on s
  * still uses p, so p may go to later work on s, but to other streams only
  * once that work has completed (PyTorch's caching allocator and

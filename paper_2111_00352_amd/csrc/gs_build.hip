@@ -31,26 +31,59 @@ inline unsigned grid_for(int64_t n, int per_block = kTB)
 
 enum : int { kFlagIndex = 1, kFlagZero = 2, kFlagUnsorted = 4, kFlagDup = 8 };
 
+// Entry k against its predecessor: index range, explicit zero, strict
+// (row, col) order.
+__device__ __forceinline__ int check_entry(int32_t r, int32_t c, float v, int32_t pr, int32_t pc, bool has_prev,
+                                           int64_t R, int64_t C)
+{
+    int f = 0;
+    if (r < 0 || r >= R || c < 0 || c >= C) f |= kFlagIndex;
+    if (v == 0.0f) f |= kFlagZero;
+    if (has_prev && !(pr < r || (pr == r && pc < c))) f |= kFlagUnsorted;
+    return f;
+}
+
+// Validation flags of the COO, ORed into *flags (one atomic per workgroup at
+// most, skipped when its bits are already set).  VEC: four entries per
+// thread through 16-byte loads (all three arrays 16-byte aligned); the
+// entries past the last whole quad are checked one by one.
+template <bool VEC>
 __global__ __launch_bounds__(kTB) void k_validate(const int32_t *__restrict__ row,
                                                   const int32_t *__restrict__ col,
                                                   const float *__restrict__ val, int64_t Z,
                                                   int64_t R, int64_t C, int *__restrict__ flags)
 {
+    __shared__ int red[kTB / kWave];
     int f = 0;
-    for (int64_t k = (int64_t)blockIdx.x * kTB + threadIdx.x; k < Z;
-         k += (int64_t)gridDim.x * kTB) {
-        int32_t r = row[k], c = col[k];
-        if (r < 0 || r >= R || c < 0 || c >= C) f |= kFlagIndex;
-        if (val[k] == 0.0f) f |= kFlagZero;
-        if (k > 0) {
-            int32_t pr = row[k - 1], pc = col[k - 1];
-            if (!(pr < r || (pr == r && pc < c))) f |= kFlagUnsorted;
+    const int64_t stride = (int64_t)gridDim.x * kTB;
+    int64_t tail = 0;
+    if (VEC) {
+        const int64_t nq = Z / 4;
+        for (int64_t q = (int64_t)blockIdx.x * kTB + threadIdx.x; q < nq; q += stride) {
+            const int4 r4 = reinterpret_cast<const int4 *>(row)[q];
+            const int4 c4 = reinterpret_cast<const int4 *>(col)[q];
+            const float4 v4 = reinterpret_cast<const float4 *>(val)[q];
+            const bool first = q == 0;
+            const int32_t pr = first ? 0 : row[4 * q - 1], pc = first ? 0 : col[4 * q - 1];
+            f |= check_entry(r4.x, c4.x, v4.x, pr, pc, !first, R, C);
+            f |= check_entry(r4.y, c4.y, v4.y, r4.x, c4.x, true, R, C);
+            f |= check_entry(r4.z, c4.z, v4.z, r4.y, c4.y, true, R, C);
+            f |= check_entry(r4.w, c4.w, v4.w, r4.z, c4.z, true, R, C);
         }
+        tail = nq * 4;
     }
-    // OR across the wave, one atomic per wave
+    for (int64_t k = tail + (int64_t)blockIdx.x * kTB + threadIdx.x; k < Z; k += stride)
+        f |= check_entry(row[k], col[k], val[k], k > 0 ? row[k - 1] : 0, k > 0 ? col[k - 1] : 0, k > 0, R, C);
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) f |= __shfl_xor(f, o, kWave);
-    if (lane_id() == 0 && f) atomicOr(flags, f);
+    if (lane_id() == 0) red[threadIdx.x / kWave] = f;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < kTB / kWave; w++) f |= red[w];
+        // the check may see a stale copy: then the (idempotent) atomic is issued
+        if (f && (__hip_atomic_load(flags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) & f) != f)
+            atomicOr(flags, f);
+    }
 }
 
 // ------------------------------------------------------------ radix sort
@@ -162,13 +195,28 @@ __global__ __launch_bounds__(kTB) void k_unpack_sorted(const uint64_t *__restric
 
 // row_ptr[i] = first position whose row is >= i: position k fills the
 // pointers of every row in (row[k-1], row[k]].
+// row_ptr from the sorted rows: the boundary between entries k-1 and k (k in
+// [0, Z], with row -1 before the first entry and row R after the last)
+// writes k into row_ptr of every row it starts.  Four boundaries per thread
+// through one 16-byte load (row is the library's own 256-byte aligned buffer).
 __global__ __launch_bounds__(kTB) void k_row_ptr(const int32_t *__restrict__ row, int64_t Z,
                                                  int64_t R, int32_t *__restrict__ row_ptr)
 {
-    for (int64_t k = (int64_t)blockIdx.x * kTB + threadIdx.x; k <= Z;
-         k += (int64_t)gridDim.x * kTB) {
-        int64_t lo = (k == 0) ? -1 : row[k - 1];
-        int64_t hi = (k == Z) ? R : row[k];
+    const int64_t nq = Z / 4;
+    const int64_t stride = (int64_t)gridDim.x * kTB;
+    for (int64_t q = (int64_t)blockIdx.x * kTB + threadIdx.x; q < nq; q += stride) {
+        const int4 r4 = reinterpret_cast<const int4 *>(row)[q];
+        const int32_t rv[4] = {r4.x, r4.y, r4.z, r4.w};
+        int64_t lo = q == 0 ? -1 : row[4 * q - 1];
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            for (int64_t i = lo + 1; i <= rv[j]; i++) row_ptr[i] = (int32_t)(4 * q + j);
+            lo = rv[j];
+        }
+    }
+    for (int64_t k = nq * 4 + (int64_t)blockIdx.x * kTB + threadIdx.x; k <= Z; k += stride) {
+        const int64_t lo = (k == 0) ? -1 : row[k - 1];
+        const int64_t hi = (k == Z) ? R : row[k];
         for (int64_t i = lo + 1; i <= hi; i++) row_ptr[i] = (int32_t)k;
     }
 }
@@ -730,7 +778,12 @@ void canonicalize(const gs_coo &A, bool assume_canonical, hipStream_t s, CanonCO
     DevBuf flags;
     flags.alloc(sizeof(int), s);
     GS_HIP(hipMemsetAsync(flags.p, 0, sizeof(int), s));
-    k_validate<<<elem_grid(Z), kTB, 0, s>>>(A.row, A.col, A.val, Z, R, C, flags.as<int>());
+    const bool aligned = ((reinterpret_cast<uintptr_t>(A.row) | reinterpret_cast<uintptr_t>(A.col) |
+                           reinterpret_cast<uintptr_t>(A.val)) & 15) == 0;
+    if (aligned)
+        k_validate<true><<<elem_grid(ceil_div(Z, 4)), kTB, 0, s>>>(A.row, A.col, A.val, Z, R, C, flags.as<int>());
+    else
+        k_validate<false><<<elem_grid(Z), kTB, 0, s>>>(A.row, A.col, A.val, Z, R, C, flags.as<int>());
     GS_LAUNCH_CHECK();
     int f = read_flag(flags.as<int>(), s);
     if (f & kFlagIndex) fail(GS_ERR_INDEX, "COO index outside the %lld x %lld matrix", (long long)R, (long long)C);
@@ -779,7 +832,7 @@ gs_matrix_ *csr_from_canon(CanonCOO &&c, hipStream_t s, bool plan)
         m->Z = c.Z;
         m->stream = s;
         m->row_ptr.alloc((size_t)(c.R + 1) * 4, s);
-        k_row_ptr<<<elem_grid(c.Z + 1), kTB, 0, s>>>(c.row.as<int32_t>(), c.Z, c.R,
+        k_row_ptr<<<elem_grid(ceil_div(c.Z, 4) + 1), kTB, 0, s>>>(c.row.as<int32_t>(), c.Z, c.R,
                                                      m->row_ptr.as<int32_t>());
         GS_LAUNCH_CHECK();
         m->col = std::move(c.col);
@@ -883,7 +936,7 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
                 sort_triplets(col, rows.as<int32_t>(), val, Z, C, R, cols.as<int32_t>(),
                               m->col.as<int32_t>(), m->val.as<float>(), s);
             }
-            k_row_ptr<<<elem_grid(Z + 1), kTB, 0, s>>>(cols.as<int32_t>(), Z, C, m->row_ptr.as<int32_t>());
+            k_row_ptr<<<elem_grid(ceil_div(Z, 4) + 1), kTB, 0, s>>>(cols.as<int32_t>(), Z, C, m->row_ptr.as<int32_t>());
             GS_LAUNCH_CHECK();
             m->device_bytes = need;
             break;

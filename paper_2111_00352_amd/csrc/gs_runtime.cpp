@@ -41,6 +41,10 @@ void *dev_alloc(size_t bytes, hipStream_t s)
     if (g_alloc.alloc) {
         p = g_alloc.alloc(bytes, s, g_alloc.ctx);
         if (!p) fail(GS_ERR_OOM, "device allocator returned NULL for %zu bytes", bytes);
+        if (reinterpret_cast<uintptr_t>(p) & 255) {
+            g_alloc.free(p, s, g_alloc.ctx);
+            fail(GS_ERR_INVALID_ARG, "device allocator returned memory not aligned to 256 bytes");
+        }
     } else {
         hipError_t e = hipMalloc(&p, bytes);
         if (e != hipSuccess || !p) {

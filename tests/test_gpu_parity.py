@@ -264,6 +264,57 @@ def test_invalid_coo_errors():
         assert eo.value.code == code
 
 
+def _offset_dev(a, off):
+    # a on the device, starting `off` elements into its allocation
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    buf = torch.empty(a.size + off, dtype=t.dtype, device=DEV)
+    buf[off:] = t.to(DEV)
+    return buf[off:]
+
+
+@pytest.mark.parametrize("off", [0, 1])
+def test_validation_at_every_quad_position(off):
+    # the validation reads four entries per thread through 16-byte loads when
+    # the three arrays are 16-byte aligned (off = 0), one at a time otherwise
+    # (off = 1): an error at any position of a quad, across a quad boundary
+    # or in the ragged tail is found, with the oracle's code
+    n = 4099
+    R = C = n
+    base_r = np.arange(n, dtype=np.int32)
+    base_c = np.arange(n, dtype=np.int32)
+    base_v = np.ones(n, np.float32)
+    for pos in (0, 1, 2, 3, 4, 7, 2048, 4096, 4098):
+        for kind in ("index", "zero", "order"):
+            r, c, v = base_r.copy(), base_c.copy(), base_v.copy()
+            if kind == "index":
+                c[pos] = C
+            elif kind == "zero":
+                v[pos] = 0.0
+            else:  # entry pos repeats its predecessor's (row, col): unsorted / duplicate
+                q = pos if pos > 0 else 1
+                r[q], c[q] = r[q - 1], c[q - 1]
+            with pytest.raises(oracle.OracleError) as eo:
+                oracle.canon(R, C, r, c, v)
+            d = [_offset_dev(x, off) for x in (r, c, v)]
+            assert (d[0].data_ptr() % 16 == 0) == (off == 0)
+            with pytest.raises(gs.GnnSpmmError) as e:
+                gs.build_format(*d, (R, C), "csr")
+            assert e.value.code == eo.value.code, (pos, kind)
+            if kind == "order":  # sorted input promised, then broken
+                with pytest.raises(gs.GnnSpmmError):
+                    gs.build_format(*d, (R, C), "csr", assume_canonical=True)
+
+
+@pytest.mark.parametrize("shuffle", [False, True])
+def test_unaligned_coo_arrays_build_the_same_matrix(shuffle):
+    g = graphgen.scaled(2)
+    case = _case_from_graph(g, shuffle_seed=12 if shuffle else None)
+    case.d_row, case.d_col, case.d_val = (_offset_dev(x, 1) for x in (case.row, case.col, case.val))
+    for fmt in ("csr", "coo", "ell", "bsr"):
+        check_layout(case, fmt)
+    check_features(case)
+
+
 def test_infeasible_padded_format_reports_bytes():
     R, C = 2000, 2000
     row, col, val = graphgen.dense_rows_coo(R, C, [5], seed=4, base_nnz=4000)
