@@ -5,7 +5,9 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <map>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "../../include/gnnspmm.h"
@@ -111,7 +113,7 @@ struct gs_matrix_ {
 
     // Kernel plans built once per matrix.
     // CSR: rows longer than the short-row limit, split into chunks.
-    int csr_long_thr = 0, csr_chunk = 0, coo_chunk = 0;
+    int csr_long_thr = 0, csr_chunk = 0;
     int64_t n_long_rows = 0, n_long_chunks = 0;
     gs::DevBuf long_rows;    // int32 row ids, n_long_rows
     gs::DevBuf long_first;   // int32 [n_long_rows+1] -> first partial slot of each long row
@@ -122,13 +124,19 @@ struct gs_matrix_ {
     int csr_wg_thr = 0;
     bool csr_sorted = false; // items ordered by decreasing length
     bool csr_planned = false; // plan_csr has run (a CSR built only for its features has no plan)
-    // COO: rows with no entries (zeroed by the COO kernel)
+    // COO: rows with no entries (zeroed by the COO fixup launch), and the
+    // entries with |col - row| < 4096 (which sets the number of rounds)
     int64_t n_empty_rows = 0;
     gs::DevBuf empty_rows;
-    // COO: chunk boundaries (row-aligned unless a row is longer than a chunk)
-    // and the rows split over several chunks, {row, first chunk, pieces, 0}
-    int64_t n_coo_chunks = 0, n_coo_split = 0;
-    gs::DevBuf coo_bounds, coo_split;
+    int64_t coo_local = 0;
+    // COO: range boundaries (T + 1) and the split rows, {range q that begins
+    // the row, row, later ranges the row runs into, 0}, per (T, per, S) the
+    // SpMM calls have used
+    struct CooRanges {
+        gs::DevBuf bounds, split;
+        int64_t n_split = 0;
+    };
+    std::map<std::tuple<int64_t, int64_t, int>, CooRanges> coo_ranges;
 
     // F-dependent workspace (partials / carries), grown on demand.
     gs::DevBuf work;
@@ -143,12 +151,20 @@ constexpr int kDefaultBsrBlock = 16;
 
 // Rows longer than this go through the split (multi-workgroup) CSR path.
 constexpr int kCsrLongRow = 128;
-// Chunk length of the split CSR path and of the COO segmented reduction.
+// Chunk length of the split CSR path.
 constexpr int kCsrChunk = 128;
 // Long rows up to this many entries take one workgroup on the vectorised
 // path; longer ones are split across workgroups.
 constexpr int kCsrWgRow = 1024;
-constexpr int kCooChunk = 128;
+// COO: range boundaries move to the next row start within at most kCooSnap
+// entries, and a segment's running sum is folded every kCooFold entries;
+// ranges hold at least kCooMinRange entries, and about kCooBandRange when
+// they come in several rounds (so that with the move they stay within
+// kCooFold).
+constexpr int kCooSnap = 32;
+constexpr int kCooFold = 128;
+constexpr int kCooMinRange = 64;
+constexpr int kCooBandRange = 96;
 // A 16x16 BSR block with at least this many stored columns counts as dense.
 constexpr int kBsrDenseCols = 8;
 
@@ -244,6 +260,7 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
 // Workgroups of 256 threads the device keeps resident at full occupancy
 // (compute units x 8), queried once.
 int resident_workgroups();
+int compute_units();
 // LDS bytes one workgroup may use (the device's limit), queried once.
 int64_t max_lds_bytes();
 

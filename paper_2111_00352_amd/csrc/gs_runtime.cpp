@@ -76,17 +76,19 @@ void ensure_work(gs_matrix_ &m, size_t bytes, hipStream_t s)
     m.work.alloc(bytes, s);
 }
 
-int resident_workgroups()
+int compute_units()
 {
     static int n = 0;
     if (n == 0) {
         int dev = 0, cus = 0;
         GS_HIP(hipGetDevice(&dev));
         GS_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-        n = (cus > 0 ? cus : 256) * 8;
+        n = cus > 0 ? cus : 256;
     }
     return n;
 }
+
+int resident_workgroups() { return compute_units() * 8; }
 
 int64_t max_lds_bytes()
 {

@@ -14,6 +14,7 @@
 // four interleaved accumulators), which keeps the rounding error far below
 // 1e-5 |A||X|; partial sums of split rows are combined in a fixed order, so
 // results are deterministic.
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <vector>
@@ -154,56 +155,143 @@ __global__ __launch_bounds__(kBlock) void k_csr_combine(const int32_t *__restric
 }
 
 // ---------------------------------------------------------------- COO
-// Segmented reduction over the (row, col)-sorted triplets.  Group q owns
-// entries [bounds[q], bounds[q+1]): the whole rows that start in one window
-// of CH entry positions (at most 2*CH - 1 entries), or one CH-entry piece of
-// a row longer than CH.  Row boundaries inside the
-// chunk are found with a ballot over "row differs from the previous entry";
-// a segment is written straight to Y unless its row continues into a
-// neighbouring chunk (only a split row does), in which case its partial
-// goes to a carry slot: slot H (index 0) for the chunk's first segment when
-// that row began in an earlier chunk, slot T (index 1) for the chunk's last
-// segment when its row begins here and continues.  k_coo_fixup then adds
-// each split row's carries in chunk order.
+// Segmented reduction over the (row, col)-sorted triplets.  The entries are
+// cut into T ranges of about per entries, each boundary q*per moved forward
+// to the first row start within S entries (a row of at most S entries is
+// never cut; a longer one may be), so group q's range is [snap(q*per),
+// snap((q+1)*per)) and all groups have the same work, within S entries,
+// whatever the row lengths.  S = per / 3 (4 to 32) when most entries lie
+// near the diagonal, where rows are short and alike; else 0, exact ranges.  T is one round of the lane groups resident on the chip, or,
+// when most entries lie near the diagonal, as many rounds as give ranges of
+// about 110 entries: the groups at work at any moment then cover one band
+// of rows, which share their X rows in L2.
+// Row boundaries inside a range are found with a ballot over "row differs
+// from the previous entry"; a segment is written straight to Y unless its
+// row continues into a neighbouring range, in which case its partial goes to
+// a carry slot: slot H (index 0) for the range's first segment when that row
+// began in an earlier range, slot T (index 1) for the range's last segment
+// when its row begins there and continues.  Inside a segment the running sum
+// is folded every CH entries into a second sum (FOLD: only when a range can
+// hold more than CH entries), so no fp32 chain is longer than CH plus the
+// number of folds.  The boundaries, and for each range the split row it
+// begins (its last row, continuing past it, or -1) with the number of later
+// ranges the row runs into, depend only on the matrix and (T, per, S):
+// they are computed once per handle and key.  k_coo_fixup then adds each
+// split row's carries in range order.
 
-template <int VEC>
-__device__ __forceinline__ void coo_flush(const Acc<VEC> &acc, int64_t row, bool first_seg,
-                                          bool last_seg, bool head_cont, bool tail_cont,
-                                          int64_t q, float *__restrict__ Y, int64_t ldy,
-                                          float *__restrict__ work, int64_t F, int64_t c0,
-                                          bool active)
+// Range boundaries b[q] = the first row start in [q*per, q*per + S] (Z
+// counts as one) or q*per itself, for q in [0, T] (b[0] = 0, b[T] = Z); then
+// the split row each range begins: its last row when that row continues
+// past the range and did not begin before it, else -1.
+__global__ __launch_bounds__(kBlock) void k_coo_bounds(const int32_t *__restrict__ row, int64_t Z, int64_t per,
+                                                       int S, int64_t T, int32_t *__restrict__ bounds)
 {
-    if (!active) return;
-    if (first_seg && head_cont)
-        st_vec<VEC>(work + (q * 2 + 0) * F + c0, acc.vec());
-    else if (last_seg && tail_cont)
-        st_vec<VEC>(work + (q * 2 + 1) * F + c0, acc.vec());
-    else
-        st_vec_stream<VEC>(Y + row * ldy + c0, acc.vec());
+    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q <= T; q += (int64_t)gridDim.x * kBlock) {
+        const int64_t p = q * per;
+        int64_t b = p <= 0 ? 0 : p >= Z ? Z : -1;
+        if (b < 0) {
+            const int64_t lim = p + S < Z ? p + S : Z;
+            b = p;
+            for (int64_t k = p; k <= lim; k++)
+                if (k == Z || row[k] != row[k - 1]) {
+                    b = k;
+                    break;
+                }
+        }
+        bounds[q] = (int32_t)b;
+    }
 }
 
-template <int VEC, int G>
+__global__ __launch_bounds__(kBlock) void k_coo_split_rows(const int32_t *__restrict__ row, int64_t Z, int64_t T,
+                                                           const int32_t *__restrict__ bounds,
+                                                           int4 *__restrict__ split, int32_t *__restrict__ flag)
+{
+    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < T; q += (int64_t)gridDim.x * kBlock) {
+        const int64_t k0 = bounds[q], k1 = bounds[q + 1];
+        int4 d = make_int4((int)q, -1, 0, 0);
+        if (k0 < k1 && k1 < Z && row[k1] == row[k1 - 1] && !(k0 > 0 && row[k0 - 1] == row[k1 - 1])) {
+            // row r continues into ranges q+1 .. q+n: those whose first entry
+            // is r (a prefix of the later ranges, found by bisection)
+            const int32_t r = row[k1 - 1];
+            int64_t lo = q + 1, hi = T;  // ranges q+1 .. lo-1 open with r; hi and later do not
+            while (lo < hi) {
+                const int64_t mid = (lo + hi) >> 1;
+                const int64_t b = bounds[mid];
+                if (b < Z && row[b] == r)
+                    lo = mid + 1;
+                else
+                    hi = mid;
+            }
+            d = make_int4((int)q, r, (int)(lo - q - 1), 0);
+        }
+        split[q] = d;
+        flag[q] = d.y >= 0;
+    }
+}
+
+// The ranges that begin a split row, in range order: split[q] for the q
+// with flag (exclusive prefix pos).
+__global__ __launch_bounds__(kBlock) void k_coo_split_list(const int4 *__restrict__ split, int64_t T,
+                                                           const int32_t *__restrict__ pos,
+                                                           int4 *__restrict__ list)
+{
+    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < T; q += (int64_t)gridDim.x * kBlock)
+        if (pos[q + 1] > pos[q]) list[pos[q]] = split[q];
+}
+
+template <int VEC>
+__device__ __forceinline__ void coo_flush(const Acc<VEC> &acc, const Acc<VEC> &tot, bool folded, int64_t row,
+                                          bool first_seg, bool last_seg, bool head_cont, bool tail_cont,
+                                          int64_t q, float *__restrict__ Y, int64_t ldy,
+                                          float *__restrict__ work, int64_t F, int64_t c0, bool active)
+{
+    if (!active) return;
+    Acc<VEC> v = acc;
+    if (folded) {
+        v = tot;
+        v.add(acc);
+    }
+    if (first_seg && head_cont)
+        st_vec<VEC>(work + (q * 2 + 0) * F + c0, v.vec());
+    else if (last_seg && tail_cont)
+        st_vec<VEC>(work + (q * 2 + 1) * F + c0, v.vec());
+    else
+        st_vec_stream<VEC>(Y + row * ldy + c0, v.vec());
+}
+
+template <int VEC, int G, bool FOLD>
 __global__ __launch_bounds__(kBlock) void k_coo_main(int64_t Z, const int32_t *__restrict__ row,
                                                      const int32_t *__restrict__ col,
                                                      const float *__restrict__ val,
                                                      const float *__restrict__ X, int64_t ldx,
                                                      float *__restrict__ Y, int64_t ldy, int64_t F,
-                                                     const int32_t *__restrict__ bounds, int64_t n_chunks,
-                                                     float *__restrict__ work)
+                                                     const int32_t *__restrict__ bounds, int64_t per,
+                                                     int64_t T, float *__restrict__ work)
 {
     constexpr int GPB = kBlock / G;
     const int g = threadIdx.x / G, lane = threadIdx.x % G;
     const int64_t c0 = (int64_t)blockIdx.y * (G * VEC) + (int64_t)lane * VEC;
     const bool active = c0 < F;
     const int64_t q = xcd_tile(blockIdx.x, gridDim.x) * GPB + g;
-    if (q >= n_chunks) return;
-    const int64_t k0 = bounds[q], k1 = bounds[q + 1];
+    if (q >= T) return;
+    const int gbase = (threadIdx.x % kWave) / G * G;  // first lane of this group in the wave
+    int64_t k0, k1;
+    if (bounds) {
+        k0 = bounds[q];
+        k1 = bounds[q + 1];
+    } else {  // exact ranges
+        k0 = q * per < Z ? q * per : Z;
+        k1 = k0 + per < Z ? k0 + per : Z;
+    }
+    if (k0 >= k1) return;
     const bool head_cont = k0 > 0 && row[k0 - 1] == row[k0];
     const bool tail_cont = k1 < Z && row[k1] == row[k1 - 1];
-    const int gbase = (threadIdx.x % kWave) / G * G;  // first lane of this group in the wave
 
-    Acc<VEC> acc;
+    Acc<VEC> acc, tot;
     acc.zero();
+    tot.zero();
+    bool folded = false;
+    int nin = 0;  // entries in acc since the segment began or acc was last folded
     int64_t cur = row[k0];
     bool first_seg = true;
     for (int64_t kb = k0; kb < k1; kb += G) {
@@ -242,26 +330,35 @@ __global__ __launch_bounds__(kBlock) void k_coo_main(int64_t Z, const int32_t *_
                 if (j >= n) break;
                 if ((j == 0 && rs[u] != cur) || ((heads >> j) & 1ull)) {
                     // the row changes before entry j: flush the finished segment
-                    coo_flush<VEC>(acc, cur, first_seg, false, head_cont, tail_cont, q, Y, ldy,
+                    coo_flush<VEC>(acc, tot, folded, cur, first_seg, false, head_cont, tail_cont, q, Y, ldy,
                                    work, F, c0, active);
                     first_seg = false;
                     acc.zero();
+                    tot.zero();
+                    folded = false;
+                    nin = 0;
                     cur = rs[u];
                 }
                 if (active) acc.fma(vs[u], xs[u]);
+                if (FOLD && ++nin == kCooFold) {
+                    tot.add(acc);
+                    acc.zero();
+                    folded = true;
+                    nin = 0;
+                }
             }
         }
     }
-    coo_flush<VEC>(acc, cur, first_seg, true, head_cont, tail_cont, q, Y, ldy, work, F, c0,
+    coo_flush<VEC>(acc, tot, folded, cur, first_seg, true, head_cont, tail_cont, q, Y, ldy, work, F, c0,
                    active);
 }
 
-// Groups [0, n_split): split row e (the int4 {row, first chunk q, piece
-// count n, 0}) adds its carries in chunk order, slot T of chunk q and then
-// slot H of chunks q+1 .. q+n-1, eight loads in flight, and writes Y.  The
-// groups after those zero the empty rows.
+// Groups [0, n_split): split row e = {range q, row r, n, 0}: range q begins
+// row r, which continues into the next n ranges; the group adds slot T of q
+// and then slot H of q+1 .. q+n in order, sixteen loads in flight, and
+// writes Y.  The groups after those zero the empty rows.
 template <int VEC, int G>
-__global__ __launch_bounds__(kBlock) void k_coo_fixup(const int4 *__restrict__ split, int64_t n_split,
+__global__ __launch_bounds__(kBlock) void k_coo_fixup(int64_t n_split, const int4 *__restrict__ split,
                                                       const float *__restrict__ work,
                                                       const int32_t *__restrict__ empty_rows,
                                                       int64_t n_empty, float *__restrict__ Y,
@@ -273,20 +370,24 @@ __global__ __launch_bounds__(kBlock) void k_coo_fixup(const int4 *__restrict__ s
     const int64_t e = (int64_t)blockIdx.x * GPB + g;
     if (c0 >= F) return;
     if (e < n_split) {
-        const int4 d = split[e];
-        const int64_t q = d.y, n = d.z;
+        const int4 d4 = split[e];
+        const int64_t q = d4.x;
+        const int2 d = make_int2(d4.y, d4.z);
         Acc<VEC> acc;
-        acc.zero();
-        for (int64_t p0 = 0; p0 < n; p0 += 8) {
-            Vec<VEC> h[8];
+        const Vec<VEC> t = ld_vec<VEC>(work + (q * 2 + 1) * F + c0);
 #pragma unroll
-            for (int u = 0; u < 8; u++) {
-                const int64_t p = p0 + u < n ? p0 + u : n - 1;
-                h[u] = ld_vec<VEC>(work + ((q + p) * 2 + (p == 0 ? 1 : 0)) * F + c0);
+        for (int i = 0; i < VEC; i++) acc.v[i] = t.v[i];
+        constexpr int B = 16;
+        for (int64_t p0 = 1; p0 <= d.y; p0 += B) {
+            Vec<VEC> h[B];
+#pragma unroll
+            for (int u = 0; u < B; u++) {
+                const int64_t p = p0 + u <= d.y ? p0 + u : d.y;
+                h[u] = ld_vec<VEC>(work + ((q + p) * 2 + 0) * F + c0);
             }
 #pragma unroll
-            for (int u = 0; u < 8; u++) {
-                if (p0 + u >= n) break;
+            for (int u = 0; u < B; u++) {
+                if (p0 + u > d.y) break;
 #pragma unroll
                 for (int i = 0; i < VEC; i++) acc.v[i] += h[u].v[i];
             }
@@ -533,27 +634,13 @@ unsigned u32_grid(int64_t n)
     return (unsigned)(n < 1 ? 1 : n);
 }
 
-int env_int_coo(const char *name, int dflt)
-{
-    const char *v = std::getenv(name);
-    if (!v || !*v) return dflt;
-    int x = std::atoi(v);
-    return x > 0 ? x : dflt;
-}
-
 }  // namespace
 
 // --------------------------------------------------------------- plans
 
-// COO chunks follow row boundaries.  The chunk bounds are the sorted,
-// de-duplicated union of (a) for every window [q*CH, (q+1)*CH) of entry
-// positions, the first row start at or after q*CH, and (b) for every row
-// longer than CH, its start, end and CH-entry piece boundaries.  A chunk
-// then holds the whole rows that start in one window (at most 2*CH - 1
-// entries, every row at most CH) or one piece of a long row, whose partial
-// sums the fixup launch adds.  Also lists the split rows and the empty rows,
-// which the kernel must zero.  Built on the device: counts, scans, one radix
-// sort, compactions.
+// The COO plan lists the empty rows, which the SpMM must zero (the kernel
+// writes only rows that hold entries), and counts the entries near the
+// diagonal, which sets the number of rounds of ranges per SpMM.
 
 namespace {
 
@@ -565,153 +652,66 @@ inline unsigned plan_blocks(int64_t n)
     return (unsigned)(g < 1 ? 1 : g > 8192 ? 8192 : g);
 }
 
-// Smallest i in [0, n) with a[i] >= t, or n.
-__device__ __forceinline__ int64_t lower_bound_i32(const int32_t *a, int64_t n, int64_t t)
+__global__ __launch_bounds__(kPB) void k_empty_flags(const int32_t *__restrict__ rp, int64_t R,
+                                                     int32_t *__restrict__ is_empty)
 {
-    int64_t lo = 0, hi = n;
-    while (lo < hi) {
-        const int64_t mid = (lo + hi) >> 1;
-        if (a[mid] < t)
-            lo = mid + 1;
-        else
-            hi = mid;
+    for (int64_t i = (int64_t)blockIdx.x * kPB + threadIdx.x; i < R; i += (int64_t)gridDim.x * kPB)
+        is_empty[i] = rp[i + 1] == rp[i];
+}
+
+__global__ __launch_bounds__(kPB) void k_empty_list(int64_t R, const int32_t *__restrict__ off,
+                                                    int32_t *__restrict__ empty)
+{
+    for (int64_t i = (int64_t)blockIdx.x * kPB + threadIdx.x; i < R; i += (int64_t)gridDim.x * kPB)
+        if (off[i + 1] > off[i]) empty[off[i]] = (int32_t)i;
+}
+
+// Entries with |col - row| < kCooNear, one partial per workgroup.
+constexpr int64_t kCooNear = 4096;
+__global__ __launch_bounds__(kPB) void k_coo_near(const int32_t *__restrict__ row, const int32_t *__restrict__ col,
+                                                  int64_t Z, unsigned long long *__restrict__ part)
+{
+    __shared__ unsigned long long t64[kPB / kWave];
+    unsigned long long n = 0;
+    for (int64_t k = (int64_t)blockIdx.x * kPB + threadIdx.x; k < Z; k += (int64_t)gridDim.x * kPB) {
+        const int64_t d = (int64_t)col[k] - row[k];
+        n += d > -kCooNear && d < kCooNear;
     }
-    return lo;
-}
-
-__global__ __launch_bounds__(kPB) void k_coo_row_counts(const int32_t *__restrict__ rp, int64_t R, int chunk,
-                                                        int32_t *__restrict__ cand, int32_t *__restrict__ is_long,
-                                                        int32_t *__restrict__ is_empty)
-{
-    for (int64_t i = (int64_t)blockIdx.x * kPB + threadIdx.x; i < R; i += (int64_t)gridDim.x * kPB) {
-        const int len = rp[i + 1] - rp[i];
-        const bool lg = len > chunk;
-        cand[i] = lg ? (len + chunk - 1) / chunk + 1 : 0;  // start, piece boundaries, end
-        is_long[i] = lg;
-        is_empty[i] = len == 0;
-    }
-}
-
-__global__ __launch_bounds__(kPB) void k_coo_window_cands(const int32_t *__restrict__ rp, int64_t R, int64_t Z,
-                                                          int chunk, int64_t W, uint64_t *__restrict__ keys)
-{
-    for (int64_t q = (int64_t)blockIdx.x * kPB + threadIdx.x; q < W; q += (int64_t)gridDim.x * kPB) {
-        const int64_t t = q * chunk;
-        const int64_t i = t > Z ? R + 1 : lower_bound_i32(rp, R + 1, t);
-        keys[q] = (uint64_t)(i <= R ? rp[i] : Z);
-    }
-}
-
-__global__ __launch_bounds__(kPB) void k_coo_long_cands(const int32_t *__restrict__ rp, int64_t R, int chunk,
-                                                        const int32_t *__restrict__ coff, int64_t W,
-                                                        uint64_t *__restrict__ keys)
-{
-    for (int64_t i = (int64_t)blockIdx.x * kPB + threadIdx.x; i < R; i += (int64_t)gridDim.x * kPB) {
-        const int n = coff[i + 1] - coff[i];
-        const int64_t s0 = rp[i], e = rp[i + 1];
-        for (int k = 0; k < n; k++) {
-            const int64_t b = s0 + (int64_t)k * chunk;
-            keys[W + coff[i] + k] = (uint64_t)(b < e ? b : e);
-        }
-    }
-}
-
-__global__ __launch_bounds__(kPB) void k_flag_new(const uint64_t *__restrict__ keys, int64_t n,
-                                                  int32_t *__restrict__ flag)
-{
-    for (int64_t k = (int64_t)blockIdx.x * kPB + threadIdx.x; k < n; k += (int64_t)gridDim.x * kPB)
-        flag[k] = k == 0 || keys[k] != keys[k - 1];
-}
-
-__global__ __launch_bounds__(kPB) void k_compact_bounds(const uint64_t *__restrict__ keys, int64_t n,
-                                                        const int32_t *__restrict__ off,
-                                                        int32_t *__restrict__ bounds)
-{
-    for (int64_t k = (int64_t)blockIdx.x * kPB + threadIdx.x; k < n; k += (int64_t)gridDim.x * kPB)
-        if (off[k + 1] > off[k]) bounds[off[k]] = (int32_t)keys[k];
-}
-
-__global__ __launch_bounds__(kPB) void k_coo_lists(const int32_t *__restrict__ rp, int64_t R, int chunk,
-                                                   const int32_t *__restrict__ loff,
-                                                   const int32_t *__restrict__ eoff,
-                                                   const int32_t *__restrict__ bounds, int64_t nbnd,
-                                                   int4 *__restrict__ split, int32_t *__restrict__ empty)
-{
-    for (int64_t i = (int64_t)blockIdx.x * kPB + threadIdx.x; i < R; i += (int64_t)gridDim.x * kPB) {
-        if (loff[i + 1] > loff[i]) {
-            const int len = rp[i + 1] - rp[i];
-            const int64_t first = lower_bound_i32(bounds, nbnd, rp[i]);  // rp[i] is a bound
-            split[loff[i]] = make_int4((int)i, (int)first, (len + chunk - 1) / chunk, 0);
-        }
-        if (eoff[i + 1] > eoff[i]) empty[eoff[i]] = (int32_t)i;
-    }
+    n = block_sum_u64<kPB>(n, t64);
+    if (threadIdx.x == 0) part[blockIdx.x] = n;
 }
 
 }  // namespace
 
 void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s)
 {
-    const int chunk = env_int_coo("GS_COO_CHUNK", kCooChunk);
-    m.coo_chunk = chunk;
     const int64_t R = m.R, Z = m.Z;
-    DevBuf cand, lng, emp;
-    cand.alloc((size_t)(R + 1) * 4, s);
-    lng.alloc((size_t)(R + 1) * 4, s);
+    DevBuf emp, near;
     emp.alloc((size_t)(R + 1) * 4, s);
+    near.alloc(sizeof(unsigned long long) * 2049, s);
+    unsigned long long *d_near = near.as<unsigned long long>() + 2048;
+    GS_HIP(hipMemsetAsync(d_near, 0, sizeof(unsigned long long), s));
     if (R > 0) {
-        k_coo_row_counts<<<plan_blocks(R), kPB, 0, s>>>(row_ptr, R, chunk, cand.as<int32_t>(),
-                                                         lng.as<int32_t>(), emp.as<int32_t>());
+        k_empty_flags<<<plan_blocks(R), kPB, 0, s>>>(row_ptr, R, emp.as<int32_t>());
         GS_HIP(hipGetLastError());
     }
-    exclusive_scan_i32(cand.as<int32_t>(), cand.as<int32_t>(), R, true, s);
-    exclusive_scan_i32(lng.as<int32_t>(), lng.as<int32_t>(), R, true, s);
     exclusive_scan_i32(emp.as<int32_t>(), emp.as<int32_t>(), R, true, s);
-    int32_t tot[3] = {0, 0, 0};
-    GS_HIP(hipMemcpyAsync(&tot[0], cand.as<int32_t>() + R, 4, hipMemcpyDeviceToHost, s));
-    GS_HIP(hipMemcpyAsync(&tot[1], lng.as<int32_t>() + R, 4, hipMemcpyDeviceToHost, s));
-    GS_HIP(hipMemcpyAsync(&tot[2], emp.as<int32_t>() + R, 4, hipMemcpyDeviceToHost, s));
-    GS_HIP(hipStreamSynchronize(s));
-
-    const int64_t W = ceil_div(Z, (int64_t)chunk) + 1;  // the last window starts at or past Z
-    const int64_t n = W + tot[0];
-    DevBuf ka, kb, pa, pb, flag;
-    ka.alloc((size_t)n * 8, s);
-    kb.alloc((size_t)n * 8, s);
-    pa.alloc((size_t)n * 4, s);
-    pb.alloc((size_t)n * 4, s);
-    flag.alloc((size_t)(n + 1) * 4, s);
-    k_coo_window_cands<<<plan_blocks(W), kPB, 0, s>>>(row_ptr, R, Z, chunk, W, ka.as<uint64_t>());
-    GS_HIP(hipGetLastError());
-    if (tot[0]) {
-        k_coo_long_cands<<<plan_blocks(R), kPB, 0, s>>>(row_ptr, R, chunk, cand.as<int32_t>(), W,
-                                                         ka.as<uint64_t>());
+    if (Z > 0) {
+        const unsigned G = (unsigned)std::min<int64_t>(2048, ceil_div(Z, (int64_t)kPB * 8));
+        k_coo_near<<<G, kPB, 0, s>>>(m.row.as<int32_t>(), m.col.as<int32_t>(), Z, near.as<unsigned long long>());
         GS_HIP(hipGetLastError());
+        add_partials_u64(near.as<unsigned long long>(), G, d_near, s);
     }
-    std::vector<int> shifts;
-    for (int sft = 0; sft < bits_for(Z); sft += 8) shifts.push_back(sft);
-    uint64_t *keys = nullptr;
-    uint32_t *perm = nullptr;
-    radix_sort_pairs(ka.as<uint64_t>(), kb.as<uint64_t>(), pa.as<uint32_t>(), pb.as<uint32_t>(), n, shifts, s,
-                     &keys, &perm);
-    k_flag_new<<<plan_blocks(n), kPB, 0, s>>>(keys, n, flag.as<int32_t>());
-    GS_HIP(hipGetLastError());
-    exclusive_scan_i32(flag.as<int32_t>(), flag.as<int32_t>(), n, true, s);
-    int32_t nbnd = 0;
-    GS_HIP(hipMemcpyAsync(&nbnd, flag.as<int32_t>() + n, 4, hipMemcpyDeviceToHost, s));
+    int32_t n_empty = 0;
+    unsigned long long n_near = 0;
+    GS_HIP(hipMemcpyAsync(&n_empty, emp.as<int32_t>() + R, 4, hipMemcpyDeviceToHost, s));
+    GS_HIP(hipMemcpyAsync(&n_near, d_near, sizeof n_near, hipMemcpyDeviceToHost, s));
     GS_HIP(hipStreamSynchronize(s));
-
-    m.n_coo_chunks = nbnd - 1;
-    m.n_coo_split = tot[1];
-    m.n_empty_rows = tot[2];
-    m.coo_bounds.alloc((size_t)nbnd * 4, s);
-    m.coo_split.alloc((size_t)tot[1] * sizeof(int4), s);
-    m.empty_rows.alloc((size_t)tot[2] * 4, s);
-    k_compact_bounds<<<plan_blocks(n), kPB, 0, s>>>(keys, n, flag.as<int32_t>(), m.coo_bounds.as<int32_t>());
-    GS_HIP(hipGetLastError());
-    if (R > 0 && (tot[1] || tot[2])) {
-        k_coo_lists<<<plan_blocks(R), kPB, 0, s>>>(row_ptr, R, chunk, lng.as<int32_t>(), emp.as<int32_t>(),
-                                                   m.coo_bounds.as<int32_t>(), nbnd, m.coo_split.as<int4>(),
-                                                   m.empty_rows.as<int32_t>());
+    m.coo_local = (int64_t)n_near;
+    m.n_empty_rows = n_empty;
+    m.empty_rows.alloc((size_t)n_empty * 4, s);
+    if (n_empty) {
+        k_empty_list<<<plan_blocks(R), kPB, 0, s>>>(R, emp.as<int32_t>(), m.empty_rows.as<int32_t>());
         GS_HIP(hipGetLastError());
     }
 }
@@ -748,24 +748,98 @@ void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
               hipStream_t s)
 {
     const Shape sh = pick_shape(X, ldx, Y, ldy, F);
-    const int64_t n_chunks = m.n_coo_chunks;
-    if (m.n_coo_split) ensure_work(m, (size_t)n_chunks * 2 * F * 4, s);
+    const int64_t Z = m.Z;
     dispatch(sh, [&]<int VEC, int G>() {
         constexpr int GPB = kBlock / G;
-        if (n_chunks) {
-            dim3 grid(u32_grid(ceil_div(n_chunks, GPB)), (unsigned)sh.fslices);
-            k_coo_main<VEC, G><<<grid, kBlock, 0, s>>>(m.Z, m.row.as<int32_t>(), m.col.as<int32_t>(),
-                                                       m.val.as<float>(), X, ldx, Y, ldy, F,
-                                                       m.coo_bounds.as<int32_t>(), n_chunks,
-                                                       m.work.as<float>());
+        int64_t T = 0, per = 0;
+        int S = 0;
+        const int32_t *bounds = nullptr;
+        const int4 *split_list = nullptr;
+        int64_t n_split = 0;
+        if (Z > 0) {
+            // resident workgroups per CU of each variant (folding or not)
+            static const int occ_fold = [] {
+                int n = 0;
+                GS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_coo_main<VEC, G, true>, kBlock, 0));
+                return n > 0 ? n : 1;
+            }();
+            static const int occ_plain = [] {
+                int n = 0;
+                GS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_coo_main<VEC, G, false>, kBlock, 0));
+                return n > 0 ? n : 1;
+            }();
+            const bool local = 2 * m.coo_local >= Z;
+            const char *force_T = std::getenv("GS_COO_RANGES");  // tests
+            // ranges of one round of the resident lane groups (shared by the
+            // F slices); as many rounds as give ranges of about kCooBandRange
+            // entries when most entries lie near the diagonal.  Row-aligned
+            // boundaries pay where rows are short and alike (near-diagonal
+            // matrices); on random graphs the cut rows are long anyway, and
+            // exact ranges keep the single round balanced.
+            auto split = [&](int occ) {
+                const int64_t round = std::max<int64_t>(1, (int64_t)occ * compute_units() * GPB / sh.fslices);
+                const int64_t rounds = local ? std::max<int64_t>(1, Z / (round * kCooBandRange)) : 1;
+                T = std::min<int64_t>(rounds * round, ceil_div(Z, (int64_t)kCooMinRange));
+                if (force_T) T = std::max<int64_t>(1, std::atoll(force_T));
+                per = ceil_div(Z, T);
+                T = ceil_div(Z, per);  // no range past the last entry
+                // (at most kCooFold - per where that leaves 4 or more: then no
+                // range exceeds kCooFold entries and the launch needs no folds)
+                S = 0;
+                if (local) {
+                    int64_t w = std::min<int64_t>(kCooSnap, per / 3);
+                    if (kCooFold - per >= 4) w = std::min<int64_t>(w, kCooFold - per);
+                    S = (int)std::max<int64_t>(4, w);
+                }
+            };
+            split(occ_fold);
+            if (per + S <= kCooFold) split(occ_plain);  // the launch will not fold: its own occupancy
+            auto key = std::make_tuple(T, per, S);
+            auto it = m.coo_ranges.find(key);
+            if (it == m.coo_ranges.end()) {  // first call with this split: boundaries and split rows
+                gs_matrix_::CooRanges cr;
+                cr.bounds.alloc((size_t)(T + 1) * 4, s);
+                DevBuf all, pos;
+                all.alloc((size_t)T * sizeof(int4), s);
+                pos.alloc((size_t)(T + 1) * 4, s);
+                const unsigned gb = (unsigned)std::min<int64_t>(4096, ceil_div(T + 1, (int64_t)kBlock));
+                k_coo_bounds<<<gb, kBlock, 0, s>>>(m.row.as<int32_t>(), Z, per, S, T, cr.bounds.as<int32_t>());
+                GS_HIP(hipGetLastError());
+                k_coo_split_rows<<<gb, kBlock, 0, s>>>(m.row.as<int32_t>(), Z, T, cr.bounds.as<int32_t>(),
+                                                       all.as<int4>(), pos.as<int32_t>());
+                GS_HIP(hipGetLastError());
+                exclusive_scan_i32(pos.as<int32_t>(), pos.as<int32_t>(), T, true, s);
+                int32_t ns = 0;
+                GS_HIP(hipMemcpyAsync(&ns, pos.as<int32_t>() + T, 4, hipMemcpyDeviceToHost, s));
+                GS_HIP(hipStreamSynchronize(s));
+                cr.n_split = ns;
+                cr.split.alloc((size_t)ns * sizeof(int4), s);
+                if (ns) {
+                    k_coo_split_list<<<gb, kBlock, 0, s>>>(all.as<int4>(), T, pos.as<int32_t>(), cr.split.as<int4>());
+                    GS_HIP(hipGetLastError());
+                }
+                it = m.coo_ranges.emplace(key, std::move(cr)).first;
+            }
+            bounds = S ? it->second.bounds.as<int32_t>() : nullptr;  // exact ranges: q * per
+            split_list = it->second.split.as<int4>();
+            n_split = it->second.n_split;
+            if (T > 1) ensure_work(m, (size_t)T * 2 * F * 4, s);  // two carry slots of F floats per range
+            dim3 grid(u32_grid(ceil_div(T, GPB)), (unsigned)sh.fslices);
+            if (per + S > kCooFold)
+                k_coo_main<VEC, G, true><<<grid, kBlock, 0, s>>>(Z, m.row.as<int32_t>(), m.col.as<int32_t>(),
+                                                                 m.val.as<float>(), X, ldx, Y, ldy, F, bounds, per,
+                                                                 T, m.work.as<float>());
+            else
+                k_coo_main<VEC, G, false><<<grid, kBlock, 0, s>>>(Z, m.row.as<int32_t>(), m.col.as<int32_t>(),
+                                                                  m.val.as<float>(), X, ldx, Y, ldy, F, bounds, per,
+                                                                  T, m.work.as<float>());
             GS_HIP(hipGetLastError());
         }
-        const int64_t groups = m.n_coo_split + m.n_empty_rows;
+        const int64_t groups = n_split + m.n_empty_rows;
         if (groups) {
             dim3 g2(u32_grid(ceil_div(groups, GPB)), (unsigned)sh.fslices);
-            k_coo_fixup<VEC, G><<<g2, kBlock, 0, s>>>(m.coo_split.as<int4>(), m.n_coo_split,
-                                                      m.work.as<float>(), m.empty_rows.as<int32_t>(),
-                                                      m.n_empty_rows, Y, ldy, F);
+            k_coo_fixup<VEC, G><<<g2, kBlock, 0, s>>>(n_split, split_list, m.work.as<float>(),
+                                                      m.empty_rows.as<int32_t>(), m.n_empty_rows, Y, ldy, F);
             GS_HIP(hipGetLastError());
         }
     });
