@@ -355,8 +355,8 @@ __global__ __launch_bounds__(kBlock) void k_coo_main(int64_t Z, const int32_t *_
 
 // Groups [0, n_split): split row e = {range q, row r, n, 0}: range q begins
 // row r, which continues into the next n ranges; the group adds slot T of q
-// and then slot H of q+1 .. q+n in order, sixteen loads in flight, and
-// writes Y.  The groups after those zero the empty rows.
+// and then slot H of q+1 .. q+n in range order, sixteen loads in flight,
+// and writes Y.  The groups after those zero the empty rows.
 template <int VEC, int G>
 __global__ __launch_bounds__(kBlock) void k_coo_fixup(int64_t n_split, const int4 *__restrict__ split,
                                                       const float *__restrict__ work,
@@ -377,20 +377,29 @@ __global__ __launch_bounds__(kBlock) void k_coo_fixup(int64_t n_split, const int
         const Vec<VEC> t = ld_vec<VEC>(work + (q * 2 + 1) * F + c0);
 #pragma unroll
         for (int i = 0; i < VEC; i++) acc.v[i] = t.v[i];
+        // each batch of B carries is summed as a tree (zeros past the last)
+        // before it joins the running sum: a row cut across n ranges adds
+        // log2(B) + n / B terms in sequence, not n
         constexpr int B = 16;
         for (int64_t p0 = 1; p0 <= d.y; p0 += B) {
             Vec<VEC> h[B];
 #pragma unroll
             for (int u = 0; u < B; u++) {
-                const int64_t p = p0 + u <= d.y ? p0 + u : d.y;
-                h[u] = ld_vec<VEC>(work + ((q + p) * 2 + 0) * F + c0);
+                if (p0 + u <= d.y) {
+                    h[u] = ld_vec<VEC>(work + ((q + p0 + u) * 2 + 0) * F + c0);
+                } else {
+#pragma unroll
+                    for (int i = 0; i < VEC; i++) h[u].v[i] = 0.0f;
+                }
             }
 #pragma unroll
-            for (int u = 0; u < B; u++) {
-                if (p0 + u > d.y) break;
+            for (int w = 1; w < B; w <<= 1)
 #pragma unroll
-                for (int i = 0; i < VEC; i++) acc.v[i] += h[u].v[i];
-            }
+                for (int u = 0; u < B; u += 2 * w)
+#pragma unroll
+                    for (int i = 0; i < VEC; i++) h[u].v[i] += h[u + w].v[i];
+#pragma unroll
+            for (int i = 0; i < VEC; i++) acc.v[i] += h[0].v[i];
         }
         st_vec_stream<VEC>(Y + (int64_t)d.x * ldy + c0, acc.vec());
     } else {

@@ -239,6 +239,34 @@ def test_empty_and_degenerate_matrices():
             check_features(case)
 
 
+@pytest.mark.parametrize("ranges", ["", "7"])
+def test_one_row_holds_most_entries(monkeypatch, ranges):
+    # a single row of 300,000 entries among short and empty rows: CSR splits it
+    # into chunks combined in order, COO cuts it across (nearly) every range and
+    # adds the carries in range order, CSC scatters every column into one row
+    if ranges:
+        monkeypatch.setenv("GS_COO_RANGES", ranges)
+    R, C = 5000, 400_000
+    rng = np.random.default_rng(131)
+    hub = np.sort(rng.choice(C, 300_000, replace=False)).astype(np.int32)
+    rows = [np.full(hub.size, 2500, np.int32)]
+    cols = [hub]
+    for i in range(0, R, 7):
+        if i == 2500:
+            continue
+        n = int(rng.integers(0, 40))
+        rows.append(np.full(n, i, np.int32))
+        cols.append(np.sort(rng.choice(C, n, replace=False)).astype(np.int32))
+    row, col = np.concatenate(rows), np.concatenate(cols)
+    val = rng.uniform(0.5, 1.5, row.size).astype(np.float32)
+    row, col, val = graphgen.shuffled(row, col, val, 132)
+    case = Case(R, C, row, col, val)
+    for fmt in ("csr", "coo", "csc"):
+        m = case.build(fmt)
+        for F in (4, 64):
+            check_spmm(case, m, graphgen.features_x(C, F, 133 + F, "normal"))
+
+
 def test_identity_spmm_is_exact():
     n = 4097
     idx = np.arange(n, dtype=np.int32)
