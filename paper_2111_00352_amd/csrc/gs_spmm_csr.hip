@@ -133,7 +133,7 @@ __global__ __launch_bounds__(kBlock) void k_csr_rows(
 }
 
 // One group per huge row: adds the row's chunk partials (consecutive slots)
-// in slot order, eight in flight, and writes the row of Y.
+// in slot order, sixteen float4 per lane in flight, and writes the row of Y.
 template <int CPL, int G>
 __global__ __launch_bounds__(kBlock) void k_csr_combine(const int32_t *__restrict__ rows,
                                                         const int32_t *__restrict__ first,
@@ -153,25 +153,37 @@ __global__ __launch_bounds__(kBlock) void k_csr_combine(const int32_t *__restric
 #pragma unroll
     for (int i = 0; i < CPL; i++) acc[i] = 0.0f;
     const int64_t s0 = first[r], s1 = first[r + 1];
-    for (int64_t sl = s0; sl < s1; sl += 8) {
-        float4 p[8][NQ];
+    // B partials in flight, summed as a tree (zeros past the last) before
+    // they join the running sum: a row of n chunks adds log2(B) + n / B terms
+    // in sequence
+    constexpr int B = NQ >= 4 ? 4 : NQ == 2 ? 8 : 16;  // 16 float4 of partials per lane
+    for (int64_t sl = s0; sl < s1; sl += B) {
+        float4 p[B][NQ];
 #pragma unroll
-        for (int u = 0; u < 8; u++)
+        for (int u = 0; u < B; u++)
 #pragma unroll
             for (int q = 0; q < NQ; q++)
                 p[u][q] = (sl + u < s1 && qok[q])
                               ? *reinterpret_cast<const float4 *>(work + (sl + u) * F + c0 + 4 * G * q)
                               : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int u = 0; u < 8; u++)
+        for (int w = 1; w < B; w <<= 1)
 #pragma unroll
-            for (int q = 0; q < NQ; q++) {
-                if (sl + u >= s1) continue;
-                acc[4 * q] += p[u][q].x;
-                acc[4 * q + 1] += p[u][q].y;
-                acc[4 * q + 2] += p[u][q].z;
-                acc[4 * q + 3] += p[u][q].w;
-            }
+            for (int u = 0; u < B; u += 2 * w)
+#pragma unroll
+                for (int q = 0; q < NQ; q++) {
+                    p[u][q].x += p[u + w][q].x;
+                    p[u][q].y += p[u + w][q].y;
+                    p[u][q].z += p[u + w][q].z;
+                    p[u][q].w += p[u + w][q].w;
+                }
+#pragma unroll
+        for (int q = 0; q < NQ; q++) {
+            acc[4 * q] += p[0][q].x;
+            acc[4 * q + 1] += p[0][q].y;
+            acc[4 * q + 2] += p[0][q].z;
+            acc[4 * q + 3] += p[0][q].w;
+        }
     }
     store_row_stream<NQ, G>(Y + (int64_t)rows[r] * ldy + c0, qok, acc);
 }
