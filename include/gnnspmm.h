@@ -224,10 +224,10 @@ void gs_ctx_destroy(gs_ctx c); /* frees every cached matrix */
  * format the selector picks for (A, F).  `key` names the adjacency: the
  * first call with a key extracts features and builds the canonical form
  * (synchronising s); later calls with the same key reuse them and assume A
- * is unchanged.  The format is re-decided on every call (the predictor sees
- * F as an input), and a format is converted at most once per key, as the
- * paper converts only when the chosen format differs from the previous
- * layer's or epoch's.  *chosen (may be NULL) receives the format used.
+ * is unchanged.  The format is decided once per (key, F) (the predictor
+ * sees F as an input) and reused by later calls, and a format is converted
+ * at most once per key, as the paper converts only when the chosen format
+ * differs from the previous layer's or epoch's.  *chosen (may be NULL) receives the format used.
  * Arguments otherwise as gs_spmm.  A gs_ctx is not thread-safe. */
 int gs_select_and_run(gs_ctx c, uint64_t key, const gs_coo *A, const float *X, int64_t ldx,
                       float *Y, int64_t ldy, int64_t F, gs_stream s, int32_t *chosen);
@@ -237,8 +237,10 @@ int gs_select_and_run(gs_ctx c, uint64_t key, const gs_coo *A, const float *X, i
 int gs_select(gs_ctx c, uint64_t key, const gs_coo *A, int64_t F, gs_stream s, int32_t *chosen);
 
 /* Host-side statistics of the last selection made through c: time spent in
- * feature extraction, prediction and conversion (seconds, wall clock,
- * measured on the first call for a key / format). */
+ * feature extraction, prediction and conversion (seconds, wall clock;
+ * features and conversion as measured on the first call for the key /
+ * format, prediction as spent in this call, a cache lookup after the first
+ * call for a (key, F)). */
 typedef struct {
     double t_features, t_predict, t_convert;
     int32_t chosen;

@@ -188,6 +188,11 @@ struct Entry {
     uint64_t bytes[GS_NUM_FORMATS] = {0};
     int feasible = 0;
     std::unordered_map<int64_t, int> profiled;  // F -> fastest format
+    struct Prediction {
+        int fmt;
+        double scores[GS_NUM_FORMATS];
+    };
+    std::unordered_map<int64_t, Prediction> predicted;  // F -> the model's choice
     double prof_time[GS_NUM_FORMATS] = {0};
     double t_features = 0, t_convert[GS_NUM_FORMATS] = {0};
     ~Entry()
@@ -277,23 +282,33 @@ int choose(gs_ctx_ &c, Entry &e, int64_t F, const float *X, int64_t ldx, float *
             fail(GS_ERR_INFEASIBLE, "fixed format %d needs %llu bytes, over the cap", chosen,
                  (unsigned long long)e.bytes[chosen]);
     } else if (c.opts.mode == GS_SEL_MODEL) {
-        double x[kNFeat], sc[GS_NUM_FORMATS];
-        model_input(e.feat, F, x);
-        normalise(c.model, x);
-        score(c.model, x, sc);
-        double best = -1e300;
-        for (int fmt : kTieOrder) {
-            if (!(e.feasible & c.opts.formats & (1u << fmt))) continue;
-            for (int k = 0; k < c.model.k; k++)
-                if (c.model.cls_fmt[k] == fmt) {
-                    st.scores[fmt] = sc[k];
-                    if (sc[k] > best) {
-                        best = sc[k];
-                        chosen = fmt;
+        // the inputs are the key's features and F, so the choice is made
+        // once per (key, F) and reused on later calls (later epochs)
+        auto it = e.predicted.find(F);
+        if (it == e.predicted.end()) {
+            Entry::Prediction p{};
+            double x[kNFeat], sc[GS_NUM_FORMATS];
+            model_input(e.feat, F, x);
+            normalise(c.model, x);
+            score(c.model, x, sc);
+            double best = -1e300;
+            int pick = -1;
+            for (int fmt : kTieOrder) {
+                if (!(e.feasible & c.opts.formats & (1u << fmt))) continue;
+                for (int k = 0; k < c.model.k; k++)
+                    if (c.model.cls_fmt[k] == fmt) {
+                        p.scores[fmt] = sc[k];
+                        if (sc[k] > best) {
+                            best = sc[k];
+                            pick = fmt;
+                        }
                     }
-                }
+            }
+            p.fmt = pick < 0 ? GS_CSR : pick;  // the model scores no feasible format: CSR
+            it = e.predicted.emplace(F, p).first;
         }
-        if (chosen < 0) chosen = GS_CSR;  // the model scores no feasible format
+        chosen = it->second.fmt;
+        for (int f = 0; f < GS_NUM_FORMATS; f++) st.scores[f] = it->second.scores[f];
     } else {  // GS_SEL_PROFILE: the exhaustive-search reference
         auto it = e.profiled.find(F);
         if (it != e.profiled.end()) {
