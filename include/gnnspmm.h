@@ -255,7 +255,7 @@ const char *gs_last_error(void);
 
 /* ABI version of this header (incremented on incompatible change). */
 int gs_abi_version(void);
-#define GS_ABI_VERSION 2
+#define GS_ABI_VERSION 3
 
 #ifdef __cplusplus
 }
