@@ -153,6 +153,33 @@ def score_exported(trees, base_scores, Xn):
     return S
 
 
+def read_model(path):
+    """The exported model file: (min, max, base scores, class format ids,
+    trees), trees as written by ``export``."""
+    with open(path) as fh:
+        lines = [ln.split() for ln in fh if ln.strip()]
+    head = {ln[0]: ln[1:] for ln in lines[:7]}
+    assert lines[0] == ["GSMODEL", "1"], "not a model file"
+    mn = np.array([float(v) for v in head["min"]])
+    mx = np.array([float(v) for v in head["max"]])
+    base = [float(v) for v in head["base"]]
+    classes = [int(v) for v in head["classes"][1:]]
+    trees, i = [], 7
+    for _ in range(int(head["ntrees"][0])):
+        _, cls, n = lines[i]
+        nodes = [(int(f), float(t), int(l), int(r), float(v)) for f, t, l, r, v in lines[i + 1:i + 1 + int(n)]]
+        trees.append((int(cls), nodes))
+        i += 1 + int(n)
+    return mn, mx, base, classes, trees
+
+
+def model_input(f, n_blocks16, F):
+    """The predictor's input for one (matrix, F): F1..F19 (Table 2 order),
+    the 16x16 block fill, F -- as ``load`` builds it from the profiles."""
+    nnz = float(f[FEATS.index("NNZ")])
+    return list(map(float, f)) + [nnz / (256.0 * n_blocks16) if n_blocks16 > 0 else 0.0, float(F)]
+
+
 def evaluate(T, pred):
     """Geometric-mean speedup over fixed CSR and fraction of the oracle."""
     tc = T[:, 0]

@@ -513,6 +513,37 @@ def test_select_model_on_mesh_prefers_diagonals():
     assert ctx.select(1, case.d_row, case.d_col, case.d_val, (case.R, case.C), 64) == "dia"
 
 
+def test_library_predictor_matches_the_training_code():
+    # the library's predictor (feature vector, fp32-rounded min-max scaling,
+    # tree walk, tie order) against the training code's own definition of
+    # each step, on the shipped model: equal scores, the same choice
+    from paper_2111_00352_amd.selector import MODEL_PATH, train
+    mn, mx, base, classes, trees = train.read_model(MODEL_PATH)
+    names = {v: k for k, v in gs.FORMATS.items()}
+    tie = ["csr", "coo", "ell", "dia", "bsr", "csc"]
+    cases = [_case_from_graph(graphgen.scaled(k)) for k in (1, 2, 3, 4, 5)]
+    cases += [_random_case(3000, 5000, 40000, 141), _random_case(20000, 20000, 9000, 142, empty=0.5)]
+    key = 0
+    for case in cases:
+        feats = gs.extract_features(case.d_row, case.d_col, case.d_val, (case.R, case.C))
+        for F in (8, 64, 128, 256):
+            key += 1
+            x = np.array([train.model_input(feats["f"], feats["n_blocks16"], F)])
+            S = train.score_exported(trees, base, train.normalise(x, mn, mx))[0]
+            ctx = gs.SelectContext("model")
+            got = ctx.select(key, case.d_row, case.d_col, case.d_val, (case.R, case.C), F)
+            st = ctx.stats()
+            ctx.close()
+            feasible = [n for n in tie if st["feasible_mask"] >> gs.FORMATS[n] & 1]
+            score = {names[fmt]: S[k] for k, fmt in enumerate(classes)}
+            for n in feasible:
+                if n in score:
+                    assert st["scores"][n] == score[n], (case.R, F, n)
+            cand = [n for n in feasible if n in score]
+            best = max(score[n] for n in cand)
+            assert got == next(n for n in cand if score[n] == best), (case.R, F)
+
+
 def test_trained_model_choice_is_near_the_profiled_best():
     # the shipped ensemble against the exhaustive selector on unseen inputs
     ratios = []
