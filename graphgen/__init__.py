@@ -310,6 +310,23 @@ def dense_rows_coo(R: int, C: int, dense_rows, seed: int, base_nnz: int = 0):
     return row, col, val
 
 
+def band_far_coo(n: int, band=(-2, 0, 3), seed: int = 0):
+    """Canonical COO of an n x n matrix: (i, i+o) for every offset o in
+    ``band`` that stays inside the matrix, plus (i, (i + n//2) mod n), a far
+    diagonal that switches offset at row n - n//2.  Values uniform[-1,1),
+    exact zeros replaced by 1/2."""
+    rng = _rng(seed)
+    i = np.arange(n, dtype=np.int64)
+    keys = [i * n + (i + n // 2) % n]
+    for o in band:
+        ok = (i + o >= 0) & (i + o < n)
+        keys.append(i[ok] * n + i[ok] + o)
+    row, col = _canon_from_keys(np.concatenate(keys), n)
+    val = _um11(rng, row.size)
+    val[val == 0] = 0.5
+    return row, col, val
+
+
 def shuffled(row, col, val, seed: int):
     """The same triplets in a seeded random order (a non-canonical input)."""
     p = _rng(seed).permutation(row.size)

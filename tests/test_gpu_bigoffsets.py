@@ -1,0 +1,68 @@
+"""Operands past the int32 range of elements.
+
+R = C = 2^23 + 2^20 + 37 and F = 256, so X and Y hold 2.4e9 elements each:
+the gather offsets j * ldx of the top 2^20 columns, the stores row * ldy of
+the top 2^20 rows and the CSC workspace index row * F all exceed 2^31.  The
+header allows n_rows, n_cols and nnz below 2^31 with 64-bit F and strides.
+
+The matrix is a band (offsets -2, 0, 3) plus a far diagonal, so every format
+is feasible.  X repeats a seeded base of P = 4099 rows (a prime, so no
+multiple of 2^32 elements maps a row onto an equal one).  Y is pre-filled
+with NaN, so a row left unwritten fails; sampled rows (first and last, both
+sides of row 2^23 and of the far diagonal's switch, and a seeded sample) are
+checked against the oracle, which receives the sampled rows and the X rows
+they touch."""
+import numpy as np
+import pytest
+import torch
+
+import graphgen
+import oracle
+import paper_2111_00352_amd as gs
+
+pytestmark = pytest.mark.gpu
+
+N = (1 << 23) + (1 << 20) + 37
+F = 256
+P = 4099
+FMTS = ["csr", "coo", "ell", "dia", "bsr", "csc"]
+
+
+@pytest.fixture(scope="module")
+def big():
+    row, col, val = graphgen.band_far_coo(N, seed=4242)
+    base = graphgen.features_x(P, F, seed=4243)
+    rp = oracle.csr(N, row)
+    rng = np.random.default_rng(4244)
+    pick = [0, 1, 2, N - 3, N - 2, N - 1, (1 << 23) - 1, 1 << 23, (1 << 23) + 1,
+            N - N // 2 - 1, N - N // 2]
+    pick += list(rng.choice(N, size=300, replace=False))
+    rows = np.unique(np.array(pick, dtype=np.int64))
+    # the sampled rows as a small CSR over the X rows they touch
+    seg = [np.arange(rp[r], rp[r + 1]) for r in rows]
+    idx = np.concatenate(seg)
+    sub_rp = np.concatenate([[0], np.cumsum([s.size for s in seg])]).astype(np.int32)
+    cols, sub_col = np.unique(col[idx], return_inverse=True)
+    Yref, M = oracle.spmm_rows(np.arange(rows.size), sub_rp, sub_col.astype(np.int32), val[idx],
+                               base[cols % P])
+    dev = "cuda"
+    X = torch.from_numpy(base).to(dev)[torch.arange(N, device=dev) % P]
+    assert X.is_contiguous() and X.numel() > (1 << 31)
+    return dict(row=torch.from_numpy(row).to(dev), col=torch.from_numpy(col).to(dev),
+                val=torch.from_numpy(val).to(dev), X=X, rows=rows, Yref=Yref, M=M)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("fmt", FMTS)
+def test_offsets_past_int32(big, fmt):
+    m = gs.build_format(big["row"], big["col"], big["val"], (N, N), fmt)
+    Y = torch.full((N, F), float("nan"), device="cuda")
+    m.spmm(big["X"], out=Y)
+    assert not bool(torch.isnan(Y).any()), f"{fmt}: rows left unwritten"
+    Yh = Y[torch.from_numpy(big["rows"]).cuda()].cpu().numpy()
+    ok, worst = oracle.check_spmm(Yh, big["Yref"], big["M"])
+    assert ok, f"{fmt}: worst |err|/bound {worst}"
+    m.close()
+    del Y
+    torch.cuda.empty_cache()
+
