@@ -163,8 +163,8 @@ constexpr int kCsrWgRow = 1024;
 // kCooFold).
 constexpr int kCooSnap = 32;
 constexpr int kCooFold = 128;
-constexpr int kCooMinRange = 64;
-constexpr int kCooBandRange = 96;
+constexpr int kCooMinRange = 32;
+constexpr int kCooBandRange = 48;
 // A 16x16 BSR block with at least this many stored columns counts as dense.
 constexpr int kBsrDenseCols = 8;
 

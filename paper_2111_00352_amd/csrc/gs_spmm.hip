@@ -17,9 +17,12 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <map>
+#include <mutex>
 #include <vector>
 
 #include "gs_device.h"
+#include "gs_gather.h"
 #include "gs_internal.h"
 
 namespace gs {
@@ -351,6 +354,132 @@ __global__ __launch_bounds__(kBlock) void k_coo_main(int64_t Z, const int32_t *_
     }
     coo_flush<VEC>(acc, tot, folded, cur, first_seg, true, head_cont, tail_cont, q, Y, ldy, work, F, c0,
                    active);
+}
+
+// The same ranges, segments and carry slots in the lane layout of the
+// vectorised CSR kernels (F a multiple of 4, 16-byte aligned operands): lane
+// l of a group holds NQ float4 at columns c0 + 4*G*q, so the per-entry
+// shuffles and row-change tests serve 4*NQ columns of a lane instead of VEC,
+// and the X rows of UB entries (8 float4 loads per lane) are requested
+// before the first is consumed.
+template <int NQ, int G>
+__device__ __forceinline__ void coo_flush4(const float *acc, const float *tot, bool folded, int64_t row,
+                                           bool first_seg, bool last_seg, bool head_cont, bool tail_cont,
+                                           int64_t q, float *__restrict__ Y, int64_t ldy,
+                                           float *__restrict__ work, int64_t F, int64_t c0, const bool *qok)
+{
+    float v[4 * NQ];
+#pragma unroll
+    for (int i = 0; i < 4 * NQ; i++) v[i] = folded ? tot[i] + acc[i] : acc[i];
+    if (first_seg && head_cont)
+        store_row<NQ, G>(work + (q * 2 + 0) * F + c0, qok, v);
+    else if (last_seg && tail_cont)
+        store_row<NQ, G>(work + (q * 2 + 1) * F + c0, qok, v);
+    else
+        store_row_stream<NQ, G>(Y + row * ldy + c0, qok, v);
+}
+
+template <int NQ, int G, bool FOLD>
+__global__ __launch_bounds__(kBlock) void k_coo_main4(int64_t Z, const int32_t *__restrict__ row,
+                                                      const int32_t *__restrict__ col,
+                                                      const float *__restrict__ val,
+                                                      const float *__restrict__ X, int64_t ldx,
+                                                      float *__restrict__ Y, int64_t ldy, int64_t F,
+                                                      const int32_t *__restrict__ bounds, int64_t per,
+                                                      int64_t T, float *__restrict__ work)
+{
+    constexpr int GPB = kBlock / G;
+    constexpr int UB = NQ >= 4 ? 2 : NQ == 2 ? 4 : 8;
+    const int g = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t c0 = (int64_t)blockIdx.y * (4 * G * NQ) + (int64_t)lane * 4;
+    bool qok[NQ];
+#pragma unroll
+    for (int i = 0; i < NQ; i++) qok[i] = c0 + 4 * G * i < F;
+    const int64_t q = xcd_tile(blockIdx.x, gridDim.x) * GPB + g;
+    if (q >= T) return;
+    const int gbase = (threadIdx.x % kWave) / G * G;
+    int64_t k0, k1;
+    if (bounds) {
+        k0 = bounds[q];
+        k1 = bounds[q + 1];
+    } else {
+        k0 = q * per < Z ? q * per : Z;
+        k1 = k0 + per < Z ? k0 + per : Z;
+    }
+    if (k0 >= k1) return;
+    const bool head_cont = k0 > 0 && row[k0 - 1] == row[k0];
+    const bool tail_cont = k1 < Z && row[k1] == row[k1 - 1];
+
+    float acc[4 * NQ], tot[4 * NQ];
+#pragma unroll
+    for (int i = 0; i < 4 * NQ; i++) acc[i] = tot[i] = 0.0f;
+    bool folded = false;
+    int nin = 0;
+    int64_t cur = row[k0];
+    bool first_seg = true;
+    for (int64_t kb = k0; kb < k1; kb += G) {
+        const int64_t k = kb + lane;
+        int rj = -1, cj = 0;
+        float vj = 0.0f;
+        if (k < k1) {
+            rj = ld_stream(row + k);
+            cj = ld_stream(col + k);
+            vj = ld_stream(val + k);
+        }
+        const int rprev = __shfl(rj, lane == 0 ? 0 : lane - 1, G);
+        const bool starts = (k < k1) && lane > 0 && rj != rprev;
+        const unsigned long long heads =
+            (__ballot(starts) >> gbase) & (G == 64 ? ~0ull : ((1ull << G) - 1));
+        const int n = (int)((k1 - kb) < G ? (k1 - kb) : G);
+        // entries past n gather row 0 of X (cj = 0: a valid row) and are skipped
+        for (int j0 = 0; j0 < n; j0 += UB) {
+            float4 xs[UB][NQ];
+            float vs[UB];
+            int rs[UB];
+#pragma unroll
+            for (int u = 0; u < UB; u++) {
+                const int c_u = __shfl(cj, j0 + u, G);
+                vs[u] = __shfl(vj, j0 + u, G);
+                rs[u] = __shfl(rj, j0 + u, G);
+                const float *xp = X + (int64_t)c_u * ldx + c0;
+#pragma unroll
+                for (int i = 0; i < NQ; i++)
+                    xs[u][i] = qok[i] ? load_x4(xp + 4 * G * i) : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+            for (int u = 0; u < UB; u++) {
+                const int j = j0 + u;
+                if (j >= n) break;
+                if ((j == 0 && rs[u] != cur) || ((heads >> j) & 1ull)) {
+                    coo_flush4<NQ, G>(acc, tot, folded, cur, first_seg, false, head_cont, tail_cont, q, Y, ldy,
+                                      work, F, c0, qok);
+                    first_seg = false;
+#pragma unroll
+                    for (int i = 0; i < 4 * NQ; i++) acc[i] = tot[i] = 0.0f;
+                    folded = false;
+                    nin = 0;
+                    cur = rs[u];
+                }
+#pragma unroll
+                for (int i = 0; i < NQ; i++) {
+                    acc[4 * i + 0] = __builtin_fmaf(vs[u], xs[u][i].x, acc[4 * i + 0]);
+                    acc[4 * i + 1] = __builtin_fmaf(vs[u], xs[u][i].y, acc[4 * i + 1]);
+                    acc[4 * i + 2] = __builtin_fmaf(vs[u], xs[u][i].z, acc[4 * i + 2]);
+                    acc[4 * i + 3] = __builtin_fmaf(vs[u], xs[u][i].w, acc[4 * i + 3]);
+                }
+                if (FOLD && ++nin == kCooFold) {
+#pragma unroll
+                    for (int i = 0; i < 4 * NQ; i++) {
+                        tot[i] += acc[i];
+                        acc[i] = 0.0f;
+                    }
+                    folded = true;
+                    nin = 0;
+                }
+            }
+        }
+    }
+    coo_flush4<NQ, G>(acc, tot, folded, cur, first_seg, true, head_cont, tail_cont, q, Y, ldy, work, F, c0, qok);
 }
 
 // Groups [0, n_split): split row e = {range q, row r, n, 0}: range q begins
@@ -753,10 +882,86 @@ void spmm_csr(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
     });
 }
 
+namespace {
+
+using CooMainFn = void (*)(int64_t, const int32_t *, const int32_t *, const float *, const float *, int64_t,
+                           float *, int64_t, int64_t, const int32_t *, int64_t, int64_t, float *);
+
+// The main COO pass for one lane shape: its plain and folding variants, lane
+// groups per workgroup and column slices of F.
+struct CooMain {
+    CooMainFn plain = nullptr, fold = nullptr;
+    int gpb = 0;
+    int64_t fslices = 0;
+};
+
+// float4 per lane of the vectorised pass: GS_COO_CPL (columns per lane: 4, 8
+// or 16) where set.  Otherwise 8 columns per lane from F = 64 on while X fits
+// in the 256 MiB memory-side cache; an X that does not is gathered from HBM,
+// where 4 columns per lane (one wider load per X row) measured faster.
+int coo_nq(int64_t C, int64_t F)
+{
+    if (const char *e = std::getenv("GS_COO_CPL")) {
+        const int c = std::atoi(e);
+        if (c == 4 || c == 8 || c == 16) return c / 4;
+    }
+    return F >= 64 && C * F * 4 <= (256ll << 20) ? 2 : 1;
+}
+
+template <int NQ, int G>
+CooMain coo_main4()
+{
+    CooMain c;
+    c.plain = k_coo_main4<NQ, G, false>;
+    c.fold = k_coo_main4<NQ, G, true>;
+    c.gpb = kBlock / G;
+    return c;
+}
+
+CooMain pick_coo_main(const Shape &sh, int64_t C, int64_t F)
+{
+    CooMain c;
+    const int nq = sh.vec == 4 ? coo_nq(C, F) : 1;
+    if (nq > 1) {
+        const int64_t lanes = ceil_div(F, (int64_t)4 * nq);
+        const int g = lanes <= 8 ? 8 : lanes <= 16 ? 16 : lanes <= 32 ? 32 : 64;
+#define GS_C4(N, GG) \
+    if (nq == N && g == GG) c = coo_main4<N, GG>();
+        GS_C4(2, 8) GS_C4(2, 16) GS_C4(2, 32) GS_C4(2, 64)
+        GS_C4(4, 8) GS_C4(4, 16) GS_C4(4, 32) GS_C4(4, 64)
+#undef GS_C4
+        c.fslices = ceil_div(F, (int64_t)4 * g * nq);
+        return c;
+    }
+    dispatch(sh, [&]<int VEC, int G>() {
+        c.plain = k_coo_main<VEC, G, false>;
+        c.fold = k_coo_main<VEC, G, true>;
+        c.gpb = kBlock / G;
+        c.fslices = sh.fslices;
+    });
+    return c;
+}
+
+// Resident workgroups per CU of a main-pass kernel.
+int coo_occupancy(CooMainFn fn)
+{
+    static std::mutex mu;
+    static std::map<CooMainFn, int> cache;
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = cache.find(fn);
+    if (it != cache.end()) return it->second;
+    int n = 0;
+    GS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, kBlock, 0));
+    return cache[fn] = n > 0 ? n : 1;
+}
+
+}  // namespace
+
 void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
               hipStream_t s)
 {
     const Shape sh = pick_shape(X, ldx, Y, ldy, F);
+    const CooMain cm = pick_coo_main(sh, m.C, F);  // main pass; the fixup keeps the generic shape
     const int64_t Z = m.Z;
     dispatch(sh, [&]<int VEC, int G>() {
         constexpr int GPB = kBlock / G;
@@ -766,17 +971,6 @@ void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
         const int4 *split_list = nullptr;
         int64_t n_split = 0;
         if (Z > 0) {
-            // resident workgroups per CU of each variant (folding or not)
-            static const int occ_fold = [] {
-                int n = 0;
-                GS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_coo_main<VEC, G, true>, kBlock, 0));
-                return n > 0 ? n : 1;
-            }();
-            static const int occ_plain = [] {
-                int n = 0;
-                GS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_coo_main<VEC, G, false>, kBlock, 0));
-                return n > 0 ? n : 1;
-            }();
             const bool local = 2 * m.coo_local >= Z;
             const char *force_T = std::getenv("GS_COO_RANGES");  // tests
             // ranges of one round of the resident lane groups (shared by the
@@ -786,10 +980,10 @@ void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
             // matrices); on random graphs the cut rows are long anyway, and
             // exact ranges keep the single round balanced.
             auto split = [&](int occ) {
-                const int64_t round = std::max<int64_t>(1, (int64_t)occ * compute_units() * GPB / sh.fslices);
+                const int64_t round = std::max<int64_t>(1, (int64_t)occ * compute_units() * cm.gpb / cm.fslices);
                 const int64_t rounds = local ? std::max<int64_t>(1, Z / (round * kCooBandRange)) : 1;
                 T = std::min<int64_t>(rounds * round, ceil_div(Z, (int64_t)kCooMinRange));
-                if (force_T) T = std::max<int64_t>(1, std::atoll(force_T));
+                if (force_T && *force_T) T = std::max<int64_t>(1, std::atoll(force_T));
                 per = ceil_div(Z, T);
                 T = ceil_div(Z, per);  // no range past the last entry
                 // (at most kCooFold - per where that leaves 4 or more: then no
@@ -801,8 +995,8 @@ void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
                     S = (int)std::max<int64_t>(4, w);
                 }
             };
-            split(occ_fold);
-            if (per + S <= kCooFold) split(occ_plain);  // the launch will not fold: its own occupancy
+            split(coo_occupancy(cm.fold));
+            if (per + S <= kCooFold) split(coo_occupancy(cm.plain));  // the launch will not fold: its own occupancy
             auto key = std::make_tuple(T, per, S);
             auto it = m.coo_ranges.find(key);
             if (it == m.coo_ranges.end()) {  // first call with this split: boundaries and split rows
@@ -833,15 +1027,10 @@ void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
             split_list = it->second.split.as<int4>();
             n_split = it->second.n_split;
             if (T > 1) ensure_work(m, (size_t)T * 2 * F * 4, s);  // two carry slots of F floats per range
-            dim3 grid(u32_grid(ceil_div(T, GPB)), (unsigned)sh.fslices);
-            if (per + S > kCooFold)
-                k_coo_main<VEC, G, true><<<grid, kBlock, 0, s>>>(Z, m.row.as<int32_t>(), m.col.as<int32_t>(),
-                                                                 m.val.as<float>(), X, ldx, Y, ldy, F, bounds, per,
-                                                                 T, m.work.as<float>());
-            else
-                k_coo_main<VEC, G, false><<<grid, kBlock, 0, s>>>(Z, m.row.as<int32_t>(), m.col.as<int32_t>(),
-                                                                  m.val.as<float>(), X, ldx, Y, ldy, F, bounds, per,
-                                                                  T, m.work.as<float>());
+            dim3 grid(u32_grid(ceil_div(T, (int64_t)cm.gpb)), (unsigned)cm.fslices);
+            const CooMainFn fn = per + S > kCooFold ? cm.fold : cm.plain;
+            fn<<<grid, kBlock, 0, s>>>(Z, m.row.as<int32_t>(), m.col.as<int32_t>(), m.val.as<float>(), X, ldx, Y,
+                                       ldy, F, bounds, per, T, m.work.as<float>());
             GS_HIP(hipGetLastError());
         }
         const int64_t groups = n_split + m.n_empty_rows;

@@ -196,17 +196,21 @@ def test_long_and_dense_rows(fmt):
     check_spmm(case, m, X)
 
 
+@pytest.mark.parametrize("cpl", ["", "4", "16"])
 @pytest.mark.parametrize("ranges", ["", "1", "3", "50", "997"])
-def test_coo_ranges_split_rows(monkeypatch, ranges):
+def test_coo_ranges_split_rows(monkeypatch, ranges, cpl):
     # the COO kernel cuts the entries into equal ranges, each boundary moved
     # to the next row start within 32 entries, so only longer rows are cut:
     # rows at and around 32 and 128 entries (the 128-entry fold), rows cut
     # over one or dozens of ranges (997 ranges of about 3 entries, most of
     # them empty after the move), back to back, at the first and last row,
     # with empty rows between them; one range sums every row in a single
-    # pass, folding the long ones
+    # pass, folding the long ones.  Each lane layout of the main pass: the
+    # rule's choice, 4 and 16 columns per lane
     if ranges:
         monkeypatch.setenv("GS_COO_RANGES", ranges)
+    if cpl:
+        monkeypatch.setenv("GS_COO_CPL", cpl)
     lens = [300, 0, 127, 128, 129, 0, 256, 257, 1000, 1, 0, 0, 5, 128, 16, 17, 15, 640, 0, 3, 31, 32, 33, 0,
             64, 129]
     C = 2000
@@ -221,7 +225,7 @@ def test_coo_ranges_split_rows(monkeypatch, ranges):
     row, col, val = graphgen.shuffled(row, col, val, 78)
     case = Case(len(lens), C, row, col, val)
     m = case.build("coo")
-    for F in (4, 64, 132):
+    for F in (4, 64, 132, 256):
         X = graphgen.features_x(C, F, 79 + F, "normal")
         check_spmm(case, m, X)
 
