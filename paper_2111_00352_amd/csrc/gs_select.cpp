@@ -18,12 +18,14 @@
 //             nnodes lines: <feat> <threshold> <left> <right> <value>
 //             (feat -1 = leaf with score value; otherwise x[feat] < threshold
 //              goes to left, else right; node 0 is the root)
+#include <cctype>
+#include <cerrno>
 #include <chrono>
+#include <climits>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
-#include <fstream>
-#include <sstream>
 #include <string>
 #include <unordered_map>
 #include <vector>
@@ -96,44 +98,83 @@ struct Model {
     std::vector<Tree> trees;
 };
 
+// Whitespace-separated tokens of the model text.  Numbers are read with
+// strtod / strtol (the conversions the C library defines; a double rounds
+// correctly) and must fill their whole token.
+struct Tokens {
+    const char *p;
+    bool word(const char *&s, const char *&e)
+    {
+        while (*p && std::isspace((unsigned char)*p)) p++;
+        if (!*p) return false;
+        s = p;
+        while (*p && !std::isspace((unsigned char)*p)) p++;
+        e = p;
+        return true;
+    }
+    bool is(const char *w)
+    {
+        const char *s, *e;
+        return word(s, e) && (size_t)(e - s) == std::strlen(w) && std::strncmp(s, w, e - s) == 0;
+    }
+    bool num(double &v)
+    {
+        const char *s, *e;
+        if (!word(s, e)) return false;
+        char *q = nullptr;
+        v = std::strtod(s, &q);
+        return q == e;
+    }
+    bool num(int &v)
+    {
+        const char *s, *e;
+        if (!word(s, e)) return false;
+        char *q = nullptr;
+        errno = 0;
+        const long x = std::strtol(s, &q, 10);
+        if (q != e || errno != 0 || x < INT_MIN || x > INT_MAX) return false;
+        v = (int)x;
+        return true;
+    }
+};
+
 void parse_model(const std::string &text, Model &m)
 {
-    std::istringstream in(text);
-    std::string tok;
+    Tokens in{text.c_str()};
     int ver = 0, nf = 0;
     auto expect = [&](const char *w) {
-        if (!(in >> tok) || tok != w) fail(GS_ERR_MODEL, "model: expected '%s'", w);
+        if (!in.is(w)) fail(GS_ERR_MODEL, "model: expected '%s'", w);
     };
     expect("GSMODEL");
-    if (!(in >> ver) || ver != 1) fail(GS_ERR_MODEL, "model: unsupported version");
+    if (!in.num(ver) || ver != 1) fail(GS_ERR_MODEL, "model: unsupported version");
     expect("nfeat");
-    if (!(in >> nf) || nf != kNFeat) fail(GS_ERR_MODEL, "model: nfeat must be %d", kNFeat);
+    if (!in.num(nf) || nf != kNFeat) fail(GS_ERR_MODEL, "model: nfeat must be %d", kNFeat);
     expect("classes");
-    if (!(in >> m.k) || m.k < 1 || m.k > GS_NUM_FORMATS) fail(GS_ERR_MODEL, "model: bad class count");
+    if (!in.num(m.k) || m.k < 1 || m.k > GS_NUM_FORMATS) fail(GS_ERR_MODEL, "model: bad class count");
     for (int c = 0; c < m.k; c++)
-        if (!(in >> m.cls_fmt[c]) || m.cls_fmt[c] < 0 || m.cls_fmt[c] >= GS_NUM_FORMATS)
+        if (!in.num(m.cls_fmt[c]) || m.cls_fmt[c] < 0 || m.cls_fmt[c] >= GS_NUM_FORMATS)
             fail(GS_ERR_MODEL, "model: bad class format id");
     expect("min");
     for (int i = 0; i < kNFeat; i++)
-        if (!(in >> m.mn[i])) fail(GS_ERR_MODEL, "model: short min table");
+        if (!in.num(m.mn[i])) fail(GS_ERR_MODEL, "model: short min table");
     expect("max");
     for (int i = 0; i < kNFeat; i++)
-        if (!(in >> m.mx[i])) fail(GS_ERR_MODEL, "model: short max table");
+        if (!in.num(m.mx[i])) fail(GS_ERR_MODEL, "model: short max table");
     expect("base");
     for (int c = 0; c < m.k; c++)
-        if (!(in >> m.base[c])) fail(GS_ERR_MODEL, "model: short base scores");
+        if (!in.num(m.base[c])) fail(GS_ERR_MODEL, "model: short base scores");
     int nt = 0;
     expect("ntrees");
-    if (!(in >> nt) || nt < 0) fail(GS_ERR_MODEL, "model: bad tree count");
+    if (!in.num(nt) || nt < 0) fail(GS_ERR_MODEL, "model: bad tree count");
     m.trees.resize(nt);
     for (auto &t : m.trees) {
         int nn = 0;
         expect("tree");
-        if (!(in >> t.cls >> nn) || t.cls < 0 || t.cls >= m.k || nn < 1)
+        if (!in.num(t.cls) || !in.num(nn) || t.cls < 0 || t.cls >= m.k || nn < 1)
             fail(GS_ERR_MODEL, "model: bad tree header");
         t.nodes.resize(nn);
         for (auto &n : t.nodes)
-            if (!(in >> n.feat >> n.thr >> n.left >> n.right >> n.value))
+            if (!in.num(n.feat) || !in.num(n.thr) || !in.num(n.left) || !in.num(n.right) || !in.num(n.value))
                 fail(GS_ERR_MODEL, "model: short node list");
         for (int i = 0; i < nn; i++) {
             const Node &n = t.nodes[i];
@@ -383,11 +424,15 @@ int gs_ctx_create(const gs_selector_opts *o, gs_ctx *out)
             c->opts.model_path = nullptr;  // not retained
             std::string text = kBuiltinModel;
             if (r.model_path) {
-                std::ifstream f(r.model_path);
+                std::FILE *f = std::fopen(r.model_path, "rb");
                 if (!f) fail(GS_ERR_MODEL, "cannot open model file %s", r.model_path);
-                std::stringstream ss;
-                ss << f.rdbuf();
-                text = ss.str();
+                text.clear();
+                char buf[1 << 16];
+                size_t n;
+                while ((n = std::fread(buf, 1, sizeof buf, f)) > 0) text.append(buf, n);
+                const bool bad = std::ferror(f) != 0;
+                std::fclose(f);
+                if (bad) fail(GS_ERR_MODEL, "cannot read model file %s", r.model_path);
             }
             parse_model(text, c->model);
         } catch (...) {
