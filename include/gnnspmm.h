@@ -99,7 +99,9 @@ typedef struct gs_matrix_ *gs_matrix; /* opaque; owns its device arrays (the for
 typedef struct gs_ctx_ *gs_ctx;       /* opaque; per-adjacency feature/format cache + selector */
 
 /* Installs the device allocator for all later allocations (NULL restores
- * hipMalloc/hipFree).  Not thread-safe against concurrent library calls. */
+ * hipMalloc/hipFree).  Memory always goes back through the hooks that
+ * allocated it, so handles built before a change stay valid.  Not
+ * thread-safe against concurrent library calls. */
 int gs_set_allocator(const gs_allocator *a);
 
 /* Builds A in format fmt on the device (Sec. 2.2; conversion, Sec. 4).
@@ -130,7 +132,9 @@ int gs_convert(gs_matrix A, int fmt, const gs_build_opts *opts, gs_stream s, gs_
 /* SpMM, Sec. 2.1: Y = A.X, Y overwritten (Y[i,:] = 0 for an empty row i).
  * X [dev] n_cols x F, row-major, leading dimension ldx >= F; Y [dev]
  * n_rows x F, leading dimension ldy >= F; columns F..ld-1 are not touched.
- * X and Y must not overlap.  fp32 in and out; products and sums in fp32
+ * F is at most 2^24 (GS_ERR_UNSUPPORTED beyond), and each operand's span
+ * ((rows - 1) * ld + F floats) must be addressable (GS_ERR_INVALID_ARG
+ * otherwise).  X and Y must not overlap.  fp32 in and out; products and sums in fp32
  * (fused multiply-add), with every sequential chain kept short enough that
  * |Y - A.X| <= 1e-5 (|A|.|X|) + 1e-6 elementwise.  Deterministic: the same
  * inputs give bit-identical Y.  CSC is the exception: its columns scatter

@@ -2,6 +2,7 @@
 // sparse matrices (the storage formats of Sec. 2.2, SpMM of Sec. 2.1,
 // features of Sec. 4.4).  Argument checking and error translation happen
 // here; the device work lives in gs_build / gs_features / gs_spmm.
+#include <cstdint>
 #include <cstring>
 
 #include "gs_internal.h"
@@ -26,7 +27,14 @@ void check_spmm_args(const gs_matrix_ *A, const float *X, int64_t ldx, const flo
 {
     if (!A) fail(GS_ERR_INVALID_ARG, "null matrix handle");
     if (F <= 0) fail(GS_ERR_INVALID_ARG, "F must be positive (got %lld)", (long long)F);
+    if (F > (int64_t(1) << 24)) fail(GS_ERR_UNSUPPORTED, "F = %lld exceeds 2^24 columns", (long long)F);
     if (ldx < F || ldy < F) fail(GS_ERR_INVALID_ARG, "leading dimensions must be >= F");
+    // each operand spans (rows - 1) * ld + F floats; the overlap test below
+    // needs that in bytes without overflow
+    auto fits = [F](int64_t rows, int64_t ld) {
+        return rows <= 1 || (rows - 1) <= (INT64_MAX / 4 - F) / ld;
+    };
+    if (!fits(A->C, ldx) || !fits(A->R, ldy)) fail(GS_ERR_INVALID_ARG, "leading dimension too large");
     if ((A->C > 0 && !X) || (A->R > 0 && !Y)) fail(GS_ERR_INVALID_ARG, "null X or Y");
     if (A->C > 0 && A->R > 0) {
         const uintptr_t x0 = (uintptr_t)X, x1 = x0 + (uintptr_t)(((A->C - 1) * ldx + F) * 4);

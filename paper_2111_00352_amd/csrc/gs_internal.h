@@ -48,23 +48,26 @@ int guarded(Fn &&f)
 
 // --------------------------------------------------------------- memory
 
-void *dev_alloc(size_t bytes, hipStream_t s);  // throws Error{GS_ERR_OOM}
-void dev_free(void *p, hipStream_t s);
+// Allocates through the hooks installed now (recorded in *used) and frees
+// through the hooks recorded at allocation, whatever is installed later.
+void *dev_alloc(size_t bytes, hipStream_t s, gs_allocator *used);  // throws Error{GS_ERR_OOM}
+void dev_free(void *p, hipStream_t s, const gs_allocator &used);
 
 // A device buffer freed when the owner goes away.
 struct DevBuf {
     void *p = nullptr;
     size_t bytes = 0;
     hipStream_t s = nullptr;
+    gs_allocator how{};  // the hooks that allocated p
     DevBuf() = default;
     DevBuf(const DevBuf &) = delete;
     DevBuf &operator=(const DevBuf &) = delete;
-    DevBuf(DevBuf &&o) noexcept : p(o.p), bytes(o.bytes), s(o.s) { o.p = nullptr; o.bytes = 0; }
+    DevBuf(DevBuf &&o) noexcept : p(o.p), bytes(o.bytes), s(o.s), how(o.how) { o.p = nullptr; o.bytes = 0; }
     DevBuf &operator=(DevBuf &&o) noexcept
     {
         if (this != &o) {
             reset();
-            p = o.p; bytes = o.bytes; s = o.s;
+            p = o.p; bytes = o.bytes; s = o.s; how = o.how;
             o.p = nullptr; o.bytes = 0;
         }
         return *this;
@@ -74,12 +77,12 @@ struct DevBuf {
     {
         reset();
         s = st;
+        p = n ? dev_alloc(n, st, &how) : nullptr;
         bytes = n;
-        p = n ? dev_alloc(n, st) : nullptr;
     }
     void reset()
     {
-        if (p) dev_free(p, s);
+        if (p) dev_free(p, s, how);
         p = nullptr;
         bytes = 0;
     }

@@ -34,8 +34,9 @@ void hip_check(hipError_t e, const char *what)
 
 static gs_allocator g_alloc = {nullptr, nullptr, nullptr};
 
-void *dev_alloc(size_t bytes, hipStream_t s)
+void *dev_alloc(size_t bytes, hipStream_t s, gs_allocator *used)
 {
+    *used = g_alloc;
     if (bytes == 0) return nullptr;
     void *p = nullptr;
     if (g_alloc.alloc) {
@@ -55,11 +56,11 @@ void *dev_alloc(size_t bytes, hipStream_t s)
     return p;
 }
 
-void dev_free(void *p, hipStream_t s)
+void dev_free(void *p, hipStream_t s, const gs_allocator &used)
 {
     if (!p) return;
-    if (g_alloc.free) {
-        g_alloc.free(p, s, g_alloc.ctx);  // stream-ordered by contract
+    if (used.free) {
+        used.free(p, s, used.ctx);  // stream-ordered by contract
     } else {
         // the library frees temporaries while work using them may still be
         // queued on s
@@ -76,15 +77,16 @@ void ensure_work(gs_matrix_ &m, size_t bytes, hipStream_t s)
     m.work.alloc(bytes, s);
 }
 
+// Device properties, read once (thread-safe static initialisation; a failed
+// query throws and is retried on the next call).
 int compute_units()
 {
-    static int n = 0;
-    if (n == 0) {
+    static const int n = [] {
         int dev = 0, cus = 0;
         GS_HIP(hipGetDevice(&dev));
         GS_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-        n = cus > 0 ? cus : 256;
-    }
+        return cus > 0 ? cus : 256;
+    }();
     return n;
 }
 
@@ -92,13 +94,12 @@ int resident_workgroups() { return compute_units() * 8; }
 
 int64_t max_lds_bytes()
 {
-    static int64_t n = 0;
-    if (n == 0) {
+    static const int64_t n = [] {
         int dev = 0, v = 0;
         GS_HIP(hipGetDevice(&dev));
         GS_HIP(hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev));
-        n = v > 0 ? v : 65536;
-    }
+        return (int64_t)(v > 0 ? v : 65536);
+    }();
     return n;
 }
 

@@ -4,6 +4,8 @@ against the CPU oracle, on the same seeded inputs.
 Bar: conversions and integer features bit-exact; feature doubles bitwise
 equal; SpMM within |Y - Y_ref| <= 1e-5 (|A||X|) + 1e-6 elementwise.
 """
+import ctypes
+
 import numpy as np
 import pytest
 import torch
@@ -377,6 +379,47 @@ def test_spmm_argument_errors():
     big = torch.zeros((100, 8), device=DEV)
     rc = gs.lib().gs_spmm(m.handle, big.data_ptr(), 8, big[10:].data_ptr(), 8, 8, None)
     assert rc == gs.ERR_INVALID_ARG  # X and Y overlap
+    # rejected before any device access: a width past 2^24 columns, and a
+    # leading dimension whose span overflows 64-bit byte offsets
+    F = (1 << 24) + 1
+    rc = gs.lib().gs_spmm(m.handle, X.data_ptr(), F, Y.data_ptr(), F, F, None)
+    assert rc == gs.ERR_UNSUPPORTED
+    rc = gs.lib().gs_spmm(m.handle, X.data_ptr(), 1 << 61, Y.data_ptr(), 8, 8, None)
+    assert rc == gs.ERR_INVALID_ARG
+
+
+def test_buffers_return_to_the_hooks_that_allocated_them():
+    # a handle built (and given a workspace) under one set of allocator hooks
+    # and destroyed after the hooks changed returns every buffer to the hooks
+    # that allocated it
+    live, errors = {}, []
+
+    def _alloc(n, stream, _ctx):
+        p = torch.cuda.caching_allocator_alloc(int(n), stream=int(stream or 0))
+        live[p] = n
+        return p
+
+    def _free(p, _stream, _ctx):
+        if p not in live:
+            errors.append(p)
+            return
+        del live[p]
+        torch.cuda.caching_allocator_delete(int(p))
+
+    hooks = gs._Allocator(gs._ALLOC_FN(_alloc), gs._FREE_FN(_free), None)
+    assert gs.lib().gs_set_allocator(ctypes.byref(hooks)) == 0
+    try:
+        case = _random_case(300, 310, 2500, 41)
+        m = case.build("coo")
+        check_spmm(case, m, graphgen.features_x(case.C, 64, 42, "normal"))
+    finally:
+        gs._alloc_keep = None
+        gs._install_torch_allocator()
+    assert live  # the handle holds its arrays and workspace
+    m.close()
+    torch.cuda.synchronize()
+    assert not live and not errors
+    check_spmm(case, case.build("csr"), graphgen.features_x(case.C, 8, 43, "normal"))
 
 
 # -------------------------------------------------------------- conversion
