@@ -16,9 +16,8 @@
 // Lane layout: lane l of a group holds float4 q at column c0 + 4*G*q, so one
 // load instruction reads G*16 contiguous bytes of an X row.  Entries are
 // fetched G at a time (one per lane) and broadcast by shuffles; X rows are
-// gathered several at a time (32 floats per lane in flight, 8 for
-// length-sorted rows, where more resident waves pay more) before any is
-// consumed; the last batch of a row is masked with a select.  The grid is
+// gathered several at a time (8 float4 loads in flight per lane) before any
+// is consumed; the last batch of a row is masked with a select.  The grid is
 // persistent (a few workgroups per CU), long-row tiles first.
 #include <algorithm>
 #include <cmath>
@@ -62,9 +61,7 @@ __device__ __forceinline__ void gather_entries(const int32_t *__restrict__ col,
     }
 }
 
-// INF: floats of gathered X rows in flight per lane (INF / CPL entries per
-// batch, at least one).
-template <int CPL, int G, bool FULL, int INF>
+template <int CPL, int G, bool FULL>
 __global__ __launch_bounds__(kBlock) void k_csr_rows(
     int64_t n_long, const int32_t *__restrict__ long_rows, const int32_t *__restrict__ rp,
     int chunk, int64_t n_short, const int4 *__restrict__ items, const int32_t *__restrict__ col,
@@ -73,7 +70,7 @@ __global__ __launch_bounds__(kBlock) void k_csr_rows(
 {
     constexpr int GPB = kBlock / G;
     constexpr int NQ = CPL / 4;
-    constexpr int U0 = INF / CPL > 0 ? INF / CPL : 1;
+    constexpr int U0 = 32 / CPL > 0 ? 32 / CPL : 1;  // 8 float4 loads in flight per lane
     constexpr int U = U0 < G ? U0 : G;
     __shared__ float4 part[GPB][G * NQ];
     const int g = threadIdx.x / G, lane = threadIdx.x % G;
@@ -468,25 +465,10 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
         // length-sorted rows, 8 -- about one tile each -- for natural order)
         const int64_t cap = (int64_t)resident_workgroups() * env_int("GS_WG_MULT", m.csr_sorted ? 4 : 8);
         dim3 grid((unsigned)std::max<int64_t>(1, std::min(tiles, cap / slices)), (unsigned)slices);
-        auto rows = [&](auto kern) {
-            kern<<<grid, kBlock, 0, s>>>(m.n_medium_rows, m.long_rows.as<int32_t>(), m.row_ptr.as<int32_t>(),
-                                         m.csr_chunk, n_group_items, m.csr_items.as<int4>() + m.n_medium_chunks,
-                                         m.col.as<int32_t>(), m.val.as<float>(), X, ldx, Y, ldy, F,
-                                         m.work.as<float>());
-        };
-        // Length-sorted rows (skewed, mostly short) at 4 columns per lane:
-        // 2 X rows in flight per lane (51 VGPRs, 8 waves per SIMD) beat 8 in
-        // flight (86 VGPRs, 5 waves): 65.9 -> 62.2 us on a 10^5-row power-law
-        // graph, 3501 -> 3426 us on a 2x10^6-row one.  Natural order keeps 8
-        // (the mesh and block graphs measured slower with fewer).
-        if constexpr (CPL == 4) {
-            if (m.csr_sorted)
-                rows(k_csr_rows<CPL, G, FU, 8>);
-            else
-                rows(k_csr_rows<CPL, G, FU, 32>);
-        } else {
-            rows(k_csr_rows<CPL, G, FU, 32>);
-        }
+        k_csr_rows<CPL, G, FU><<<grid, kBlock, 0, s>>>(
+            m.n_medium_rows, m.long_rows.as<int32_t>(), m.row_ptr.as<int32_t>(), m.csr_chunk,
+            n_group_items, m.csr_items.as<int4>() + m.n_medium_chunks, m.col.as<int32_t>(),
+            m.val.as<float>(), X, ldx, Y, ldy, F, m.work.as<float>());
         GS_HIP(hipGetLastError());
         if (n_huge) {
             dim3 g2((unsigned)ceil_div(n_huge, GPB), (unsigned)slices);
