@@ -14,6 +14,7 @@
 // four interleaved accumulators), which keeps the rounding error far below
 // 1e-5 |A||X|; partial sums of split rows are combined in a fixed order, so
 // results are deterministic.
+#include <algorithm>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -994,6 +995,8 @@ void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
                     if (kCooFold - per >= 4) w = std::min<int64_t>(w, kCooFold - per);
                     S = (int)std::max<int64_t>(4, w);
                 }
+                if (const char *e = std::getenv("GS_COO_SNAP"); e && *e)  // tests and tuning
+                    S = (int)std::clamp<int64_t>(std::atoll(e), 0, kCooSnap);
             };
             split(coo_occupancy(cm.fold));
             if (per + S <= kCooFold) split(coo_occupancy(cm.plain));  // the launch will not fold: its own occupancy

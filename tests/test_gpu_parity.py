@@ -213,6 +213,24 @@ def test_coo_ranges_split_rows(monkeypatch, ranges, cpl):
         monkeypatch.setenv("GS_COO_RANGES", ranges)
     if cpl:
         monkeypatch.setenv("GS_COO_CPL", cpl)
+    _check_coo_row_mix()
+
+
+@pytest.mark.parametrize("cpl", ["", "16"])
+@pytest.mark.parametrize("snap", ["4", "32"])
+@pytest.mark.parametrize("ranges", ["50", "997"])
+def test_coo_snapped_boundaries(monkeypatch, ranges, snap, cpl):
+    # the same rows with boundaries moved to the next row start within 4 or
+    # 32 entries (the near-diagonal rule, forced on this random pattern):
+    # ranges that grow past the fold length, ranges left empty by the move
+    monkeypatch.setenv("GS_COO_RANGES", ranges)
+    monkeypatch.setenv("GS_COO_SNAP", snap)
+    if cpl:
+        monkeypatch.setenv("GS_COO_CPL", cpl)
+    _check_coo_row_mix()
+
+
+def _check_coo_row_mix():
     lens = [300, 0, 127, 128, 129, 0, 256, 257, 1000, 1, 0, 0, 5, 128, 16, 17, 15, 640, 0, 3, 31, 32, 33, 0,
             64, 129]
     C = 2000
