@@ -66,3 +66,59 @@ def test_offsets_past_int32(big, fmt):
     del Y
     torch.cuda.empty_cache()
 
+
+
+# The largest entry count the header allows: 2^27 - 5 rows with 16 band
+# entries each (edges clipped), 2^31 - 329 entries.  Entry indices, row
+# pointers, range bounds, radix-sort positions and the CSC permutation then
+# run up to the top of the int32 range.  The padded formats exceed the
+# default 8 GiB cap at this size, so the unpadded ones are run, with F = 4.
+NZ_ROWS = (1 << 27) - 5
+NZ_OFFS = np.array([-7, -5, -3, -2, -1, 0, 1, 2, 3, 5, 8, 13, 21, 34, 55, 89], np.int32)
+
+
+@pytest.fixture(scope="module")
+def most_entries():
+    n = NZ_ROWS
+    row = np.repeat(np.arange(n, dtype=np.int32), NZ_OFFS.size)
+    col = row + np.tile(NZ_OFFS, n)
+    keep = (col >= 0) & (col < n)
+    row, col = row[keep], col[keep]
+    del keep
+    assert row.size == (1 << 31) - 329
+    # values k/2^16 + 1/2 for k = entry index mod 2^16: exact, never zero
+    val = (np.arange(row.size, dtype=np.uint32) & 0xFFFF).astype(np.float32) * np.float32(2.0**-16)
+    val += np.float32(0.5)
+    X = graphgen.features_x(n, 4, seed=4245)
+    rng = np.random.default_rng(4246)
+    pick = [0, 1, 7, 88, 89, n // 2, n - 90, n - 89, n - 8, n - 1]
+    pick += list(rng.choice(n, size=200, replace=False))
+    rows = np.unique(np.array(pick, dtype=np.int64))
+    starts = np.searchsorted(row, rows)
+    ends = np.searchsorted(row, rows, side="right")
+    seg = [np.arange(s, e) for s, e in zip(starts, ends)]
+    idx = np.concatenate(seg)
+    sub_rp = np.concatenate([[0], np.cumsum([s.size for s in seg])]).astype(np.int32)
+    cols, sub_col = np.unique(col[idx], return_inverse=True)
+    Yref, M = oracle.spmm_rows(np.arange(rows.size), sub_rp, sub_col.astype(np.int32), val[idx], X[cols])
+    dev = "cuda"
+    out = dict(row=torch.from_numpy(row).to(dev), col=torch.from_numpy(col).to(dev),
+               val=torch.from_numpy(val).to(dev), X=torch.from_numpy(X).to(dev), rows=rows, Yref=Yref, M=M)
+    del row, col, val
+    return out
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("fmt", ["csr", "coo", "csc"])
+def test_most_entries(most_entries, fmt):
+    b = most_entries
+    m = gs.build_format(b["row"], b["col"], b["val"], (NZ_ROWS, NZ_ROWS), fmt)
+    Y = torch.full((NZ_ROWS, 4), float("nan"), device="cuda")
+    m.spmm(b["X"], out=Y)
+    assert not bool(torch.isnan(Y).any()), f"{fmt}: rows left unwritten"
+    Yh = Y[torch.from_numpy(b["rows"]).cuda()].cpu().numpy()
+    ok, worst = oracle.check_spmm(Yh, b["Yref"], b["M"])
+    assert ok, f"{fmt}: worst |err|/bound {worst}"
+    m.close()
+    del Y
+    torch.cuda.empty_cache()
