@@ -122,3 +122,67 @@ def test_most_entries(most_entries, fmt):
     m.close()
     del Y
     torch.cuda.empty_cache()
+
+
+def _band_aggregates(n, offs):
+    """Integer aggregates of the n x n matrix with entries (i, i+o), o in offs,
+    worked out from the band's geometry: every row and column away from the
+    edges holds len(offs) entries, and the 16x16 block pattern of a block row
+    repeats along the band, so only the first and last rows and block rows
+    are enumerated."""
+    offs = [int(o) for o in offs]
+    k = len(offs)
+    edge = max(abs(o) for o in offs) + 1
+    assert n > 2 * edge  # every offset then has entries, and the ends do not meet
+
+    def counts(sign):  # entries of line i: offsets with 0 <= i + sign*o < n
+        idx = list(range(min(edge, n))) + list(range(max(edge, n - edge), n))
+        c = {i: sum(1 for o in offs if 0 <= i + sign * o < n) for i in idx}
+        interior = n - len(c)
+        s2 = sum(v * v for v in c.values()) + interior * k * k
+        full = [c.get(i, k) for i in range(min(edge + 1, n))] + [c.get(i, k) for i in range(max(edge + 1, n - edge - 1), n)]
+        bounce = sum(abs(full[j + 1] - full[j]) for j in range(len(full) - 1))
+        return max(c.values()), min(c.values()), s2, bounce
+
+    max_r, min_r, s2r, br = counts(+1)
+    max_c, min_c, s2c, bc = counts(-1)
+    nbr = (n + 15) // 16
+    eb = edge // 16 + 2
+
+    def blocks(b):
+        ds = set()
+        for kk in range(16):
+            i = 16 * b + kk
+            if i >= n:
+                break
+            for o in offs:
+                if 0 <= i + o < n:
+                    ds.add((i + o) // 16)
+        return len(ds)
+
+    ends = sorted(set(range(min(eb, nbr))) | set(range(max(0, nbr - eb), nbr)))
+    nb16 = sum(blocks(b) for b in ends) + (nbr - len(ends)) * blocks(nbr // 2)
+    return {"n_rows": n, "n_cols": n, "n_diags": k, "max_rd": max_r, "min_rd": min_r, "max_cd": max_c,
+            "min_cd": min_c, "sum_rd2": s2r, "sum_cd2": s2c, "bounce_r": br, "bounce_c": bc,
+            "n_blocks16": nb16}
+
+
+def test_band_aggregates_match_the_oracle_on_a_small_band():
+    # the closed forms above, checked against the oracle where it is fast
+    n = 1000
+    row = np.repeat(np.arange(n, dtype=np.int32), NZ_OFFS.size)
+    col = row + np.tile(NZ_OFFS, n)
+    keep = (col >= 0) & (col < n)
+    ints, _ = oracle.features(n, n, row[keep], col[keep])
+    exp = _band_aggregates(n, NZ_OFFS)
+    exp["nnz"] = int(keep.sum())
+    assert ints == exp
+
+
+@pytest.mark.timeout(600)
+def test_features_at_most_entries(most_entries):
+    b = most_entries
+    got = gs.extract_features(b["row"], b["col"], b["val"], (NZ_ROWS, NZ_ROWS))
+    exp = _band_aggregates(NZ_ROWS, NZ_OFFS)
+    exp["nnz"] = (1 << 31) - 329
+    assert {k: got[k] for k in exp} == exp
