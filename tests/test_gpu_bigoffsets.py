@@ -71,8 +71,9 @@ def test_offsets_past_int32(big, fmt):
 # The largest entry count the header allows: 2^27 - 5 rows with 16 band
 # entries each (edges clipped), 2^31 - 329 entries.  Entry indices, row
 # pointers, range bounds, radix-sort positions and the CSC permutation then
-# run up to the top of the int32 range.  The padded formats exceed the
-# default 8 GiB cap at this size, so the unpadded ones are run, with F = 4.
+# run up to the top of the int32 range; ELL's K*R slots and DIA's data pass
+# 2^31.  The padded formats exceed the default 8 GiB cap at this size, so
+# ELL and DIA are built under a 40 GiB cap (BSR would need about 60 GB).
 NZ_ROWS = (1 << 27) - 5
 NZ_OFFS = np.array([-7, -5, -3, -2, -1, 0, 1, 2, 3, 5, 8, 13, 21, 34, 55, 89], np.int32)
 
@@ -109,18 +110,23 @@ def most_entries():
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("fmt", ["csr", "coo", "csc"])
+@pytest.mark.parametrize("fmt", ["csr", "coo", "csc", "ell", "dia"])
 def test_most_entries(most_entries, fmt):
     b = most_entries
-    m = gs.build_format(b["row"], b["col"], b["val"], (NZ_ROWS, NZ_ROWS), fmt)
+    m = gs.build_format(b["row"], b["col"], b["val"], (NZ_ROWS, NZ_ROWS), fmt, max_bytes=40 << 30)
     Y = torch.full((NZ_ROWS, 4), float("nan"), device="cuda")
     m.spmm(b["X"], out=Y)
     assert not bool(torch.isnan(Y).any()), f"{fmt}: rows left unwritten"
     Yh = Y[torch.from_numpy(b["rows"]).cuda()].cpu().numpy()
+    del Y
     ok, worst = oracle.check_spmm(Yh, b["Yref"], b["M"])
     assert ok, f"{fmt}: worst |err|/bound {worst}"
+    if fmt in ("ell", "dia"):  # the padded layouts give back the canonical COO, bit for bit
+        r, c, v = m.to_coo()
+        assert torch.equal(r, b["row"]) and torch.equal(c, b["col"])
+        assert torch.equal(v.view(torch.int32), b["val"].view(torch.int32))
+        del r, c, v
     m.close()
-    del Y
     torch.cuda.empty_cache()
 
 
