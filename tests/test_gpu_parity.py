@@ -424,6 +424,7 @@ def test_buffers_return_to_the_hooks_that_allocated_them():
         del live[p]
         torch.cuda.caching_allocator_delete(int(p))
 
+    gs._require_gpu()  # the binding installs its own hooks on first use: do that before replacing them
     hooks = gs._Allocator(gs._ALLOC_FN(_alloc), gs._FREE_FN(_free), None)
     assert gs.lib().gs_set_allocator(ctypes.byref(hooks)) == 0
     try:
@@ -438,6 +439,41 @@ def test_buffers_return_to_the_hooks_that_allocated_them():
     torch.cuda.synchronize()
     assert not live and not errors
     check_spmm(case, case.build("csr"), graphgen.features_x(case.C, 8, 43, "normal"))
+
+
+def test_work_stays_on_the_callers_stream():
+    # Everything on a second stream (default priority), queued behind an
+    # asynchronous copy of X into a fresh buffer on that stream: builds,
+    # SpMMs, a conversion, features and the selector.  A kernel launched on
+    # another stream could read X before the copy lands.  Results are read
+    # after synchronising that stream alone.
+    case = _random_case(3000, 2800, 60000, 61)
+    F = 64
+    X = graphgen.features_x(case.C, F, 62, "normal")
+    Xpin = torch.from_numpy(X).pin_memory()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())  # the case's arrays were copied on the default stream
+    with torch.cuda.stream(s):
+        Xd = torch.empty((case.C, F), device=DEV)
+        Xd.copy_(Xpin, non_blocking=True)
+        outs = []
+        for fmt in FMTS:
+            m = case.build(fmt)
+            outs.append((fmt, m, m.spmm(Xd)))
+        m2 = outs[0][1].convert("ell")
+        outs.append(("csr->ell", m2, m2.spmm(Xd)))
+        feats = gs.extract_features(case.d_row, case.d_col, case.d_val, (case.R, case.C))
+        sel = []
+        for mode in ("profile", "model"):
+            ctx = gs.SelectContext(mode)
+            sel.append((mode, ctx, *ctx.run(9, case.d_row, case.d_col, case.d_val, (case.R, case.C), Xd)))
+    s.synchronize()
+    Yref, M = oracle.spmm(case.R, case.rp, case.ccol, case.cval, X)
+    for name, _, Y in outs + [(f"select/{mode}/{fmt}", ctx, Y) for mode, ctx, Y, fmt in sel]:
+        ok, worst = oracle.check_spmm(_host(Y), Yref, M)
+        assert ok, f"{name}: worst |err|/bound {worst}"
+    ints, f = oracle.features(case.R, case.C, case.crow, case.ccol)
+    assert all(feats[k] == v for k, v in ints.items()) and feats["f"] == f.tolist()
 
 
 # -------------------------------------------------------------- conversion
