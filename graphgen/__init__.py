@@ -381,13 +381,17 @@ def training_matrix(i: int):
 
 
 def structured_matrix(i: int):
-    """Structured training matrix i (0..119): banded, community-block,
-    power-law and grid patterns at 10^4..2x10^5 rows, values 1."""
+    """Structured training matrix i: banded, community-block, power-law and
+    grid patterns, values 1.  Matrices 0..119 have 10^4..2x10^5 rows,
+    matrices 120..159 have 2x10^5..1.5x10^6 (the sizes of large GNN graphs;
+    banded ones then keep at most 30 diagonals, power-law ones have expected
+    degrees capped at 1..8 x sqrt(n deg) instead of sqrt(n deg))."""
     rng = _rng(60_000 + i)
     kind = ("banded", "blocks", "powerlaw", "grid")[i % 4]
-    n = int(np.exp(rng.uniform(np.log(1e4), np.log(2e5))))
+    lo, hi = (1e4, 2e5) if i < 120 else (2e5, 1.5e6)
+    n = int(np.exp(rng.uniform(np.log(lo), np.log(hi))))
     if kind == "banded":
-        nd = int(rng.integers(1, 40))
+        nd = int(rng.integers(1, 40 if i < 120 else 30))
         offs = np.unique(rng.integers(-n // 8, n // 8, size=nd))
         keys = []
         for o in offs:
@@ -412,7 +416,10 @@ def structured_matrix(i: int):
     elif kind == "powerlaw":
         gamma = rng.uniform(1.8, 3.0)
         deg = rng.uniform(3, 30)
-        u, v = _chung_lu_pairs(rng, n, gamma, deg, int(np.sqrt(n * deg)))
+        cap = np.sqrt(n * deg)
+        if i >= 120:  # hub-heavy too: expected degrees capped at 1..8 x sqrt(n deg)
+            cap *= rng.uniform(1.0, 8.0)
+        u, v = _chung_lu_pairs(rng, n, gamma, deg, int(cap))
         row, col = _sym_with_self(u, v, n)
     else:
         m = int(np.sqrt(n))

@@ -46,7 +46,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("out")
     ap.add_argument("--random", type=int, default=300)
-    ap.add_argument("--structured", type=int, default=120)
+    ap.add_argument("--structured", type=int, default=160)
     ap.add_argument("--reps", type=int, default=5)
     ap.add_argument("--start", type=int, default=0, help="first job (to split a collection)")
     ap.add_argument("--count", type=int, default=None, help="number of jobs from --start")

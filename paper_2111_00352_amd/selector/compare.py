@@ -8,7 +8,7 @@ inference time, accuracy and realised speedup) and against an MLP, 1-nearest
 neighbour and an SVM (Sec. 6.4, accuracy and prediction time).  Every
 candidate here sees the same inputs (Table 2 features plus the 16x16 block
 fill and F, min-max scaled with the training fold's range and clipped) and
-the same labels (Eq. 1 with w = 1, 1% ties) as ``train``, and is scored with
+the same labels (Eq. 1 with w = 1, 3% ties) as ``train``, and is scored with
 the same grouped k-fold split (no matrix in both the training and the test
 fold) on:
   * accuracy against the profiled label;
