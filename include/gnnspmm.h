@@ -213,7 +213,7 @@ typedef enum {
 typedef struct {
     int32_t mode;           /* gs_sel_mode */
     int32_t fixed;          /* gs_format for GS_SEL_FIXED */
-    const char *model_path; /* [host] model file for GS_SEL_MODEL; NULL = built-in model */
+    const char *model_path; /* [host] model file, read only for GS_SEL_MODEL; NULL = built-in model */
     uint64_t max_bytes;     /* formats whose padded size exceeds this are never chosen; 0 -> 8 GiB */
     int32_t bsr_block;      /* 0 -> 16 */
     int32_t profile_reps;   /* timed runs per format for GS_SEL_PROFILE; 0 -> 3 */

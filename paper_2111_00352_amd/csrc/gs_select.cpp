@@ -103,12 +103,13 @@ struct Model {
 // correctly) and must fill their whole token.
 struct Tokens {
     const char *p;
+    static bool space(char c) { return c == ' ' || c == '\n' || c == '\t' || c == '\r' || c == '\v' || c == '\f'; }
     bool word(const char *&s, const char *&e)
     {
-        while (*p && std::isspace((unsigned char)*p)) p++;
+        while (*p && space(*p)) p++;
         if (!*p) return false;
         s = p;
-        while (*p && !std::isspace((unsigned char)*p)) p++;
+        while (*p && !space(*p)) p++;
         e = p;
         return true;
     }
@@ -125,19 +126,72 @@ struct Tokens {
         v = std::strtod(s, &q);
         return q == e;
     }
-    bool num(int &v)
+    // A hexadecimal floating-point literal as C99 and Python's float.hex()
+    // write it, [-]0xH.HHHp[+-]E: exact by construction, so it is read
+    // without a general decimal conversion.  At most 53 significant bits.
+    bool hexnum(double &v)
     {
         const char *s, *e;
         if (!word(s, e)) return false;
-        char *q = nullptr;
-        errno = 0;
-        const long x = std::strtol(s, &q, 10);
-        if (q != e || errno != 0 || x < INT_MIN || x > INT_MAX) return false;
+        const char *p = s;
+        const bool neg = *p == '-';
+        if (*p == '-' || *p == '+') p++;
+        if (e - p < 4 || p[0] != '0' || (p[1] != 'x' && p[1] != 'X')) return false;
+        p += 2;
+        uint64_t m = 0;
+        int frac = 0, nd = 0;
+        bool dot = false;
+        for (; p < e && *p != 'p' && *p != 'P'; p++) {
+            if (*p == '.') {
+                if (dot) return false;
+                dot = true;
+                continue;
+            }
+            const int d = std::isdigit((unsigned char)*p) ? *p - '0'
+                          : (*p >= 'a' && *p <= 'f') ? *p - 'a' + 10
+                          : (*p >= 'A' && *p <= 'F') ? *p - 'A' + 10
+                                                     : -1;
+            if (d < 0 || nd == 15) return false;
+            m = m * 16 + (uint64_t)d;
+            nd++;
+            if (dot) frac++;
+        }
+        long long ex;
+        if (nd == 0 || p == e || (m >> 53) != 0 || !integer(p + 1, e, -1100, 1100, ex)) return false;
+        v = std::ldexp((double)m, (int)(ex - 4 * frac));
+        if (neg) v = -v;
+        return true;
+    }
+    // A decimal integer filling [s, e), within the int range.
+    static bool integer(const char *s, const char *e, long long lo, long long hi, long long &x)
+    {
+        const bool neg = s < e && *s == '-';
+        if (s < e && (*s == '-' || *s == '+')) s++;
+        if (s == e || e - s > 11) return false;
+        x = 0;
+        for (; s < e; s++) {
+            if (*s < '0' || *s > '9') return false;
+            x = x * 10 + (*s - '0');
+        }
+        if (neg) x = -x;
+        return x >= lo && x <= hi;
+    }
+    bool num(int &v)
+    {
+        const char *s, *e;
+        long long x;
+        if (!word(s, e) || !integer(s, e, INT_MIN, INT_MAX, x)) return false;
         v = (int)x;
         return true;
     }
 };
 
+// Model file, version 1: "GSMODEL 1", "nfeat 21", "classes k id...",
+// "min x...", "max x...", "base s...", "ntrees N", then per tree
+// "tree cls nn" and nn nodes "feat thr left right value" (feat = -1 for a
+// leaf), numbers in decimal.  Version 2 is the same with every real written
+// as a hexadecimal literal and leaves as "L value", internal nodes as
+// "feat thr left right".
 void parse_model(const std::string &text, Model &m)
 {
     Tokens in{text.c_str()};
@@ -146,7 +200,8 @@ void parse_model(const std::string &text, Model &m)
         if (!in.is(w)) fail(GS_ERR_MODEL, "model: expected '%s'", w);
     };
     expect("GSMODEL");
-    if (!in.num(ver) || ver != 1) fail(GS_ERR_MODEL, "model: unsupported version");
+    if (!in.num(ver) || (ver != 1 && ver != 2)) fail(GS_ERR_MODEL, "model: unsupported version");
+    auto real = [&](double &v) { return ver == 1 ? in.num(v) : in.hexnum(v); };
     expect("nfeat");
     if (!in.num(nf) || nf != kNFeat) fail(GS_ERR_MODEL, "model: nfeat must be %d", kNFeat);
     expect("classes");
@@ -156,13 +211,13 @@ void parse_model(const std::string &text, Model &m)
             fail(GS_ERR_MODEL, "model: bad class format id");
     expect("min");
     for (int i = 0; i < kNFeat; i++)
-        if (!in.num(m.mn[i])) fail(GS_ERR_MODEL, "model: short min table");
+        if (!real(m.mn[i])) fail(GS_ERR_MODEL, "model: short min table");
     expect("max");
     for (int i = 0; i < kNFeat; i++)
-        if (!in.num(m.mx[i])) fail(GS_ERR_MODEL, "model: short max table");
+        if (!real(m.mx[i])) fail(GS_ERR_MODEL, "model: short max table");
     expect("base");
     for (int c = 0; c < m.k; c++)
-        if (!in.num(m.base[c])) fail(GS_ERR_MODEL, "model: short base scores");
+        if (!real(m.base[c])) fail(GS_ERR_MODEL, "model: short base scores");
     int nt = 0;
     expect("ntrees");
     if (!in.num(nt) || nt < 0) fail(GS_ERR_MODEL, "model: bad tree count");
@@ -173,9 +228,23 @@ void parse_model(const std::string &text, Model &m)
         if (!in.num(t.cls) || !in.num(nn) || t.cls < 0 || t.cls >= m.k || nn < 1)
             fail(GS_ERR_MODEL, "model: bad tree header");
         t.nodes.resize(nn);
-        for (auto &n : t.nodes)
-            if (!in.num(n.feat) || !in.num(n.thr) || !in.num(n.left) || !in.num(n.right) || !in.num(n.value))
-                fail(GS_ERR_MODEL, "model: short node list");
+        for (auto &n : t.nodes) {
+            bool ok;
+            if (ver == 1) {
+                ok = in.num(n.feat) && in.num(n.thr) && in.num(n.left) && in.num(n.right) && in.num(n.value);
+            } else {
+                const char *save = in.p;
+                if (in.is("L")) {
+                    n = Node{-1, 0.0, 0, 0, 0.0};
+                    ok = in.hexnum(n.value);
+                } else {
+                    in.p = save;
+                    n.value = 0.0;
+                    ok = in.num(n.feat) && n.feat >= 0 && in.hexnum(n.thr) && in.num(n.left) && in.num(n.right);
+                }
+            }
+            if (!ok) fail(GS_ERR_MODEL, "model: short or malformed node list");
+        }
         for (int i = 0; i < nn; i++) {
             const Node &n = t.nodes[i];
             if (n.feat >= kNFeat || n.feat < -1) fail(GS_ERR_MODEL, "model: bad feature index");
@@ -422,19 +491,21 @@ int gs_ctx_create(const gs_selector_opts *o, gs_ctx *out)
         try {
             c->opts = r;
             c->opts.model_path = nullptr;  // not retained
-            std::string text = kBuiltinModel;
-            if (r.model_path) {
-                std::FILE *f = std::fopen(r.model_path, "rb");
-                if (!f) fail(GS_ERR_MODEL, "cannot open model file %s", r.model_path);
-                text.clear();
-                char buf[1 << 16];
-                size_t n;
-                while ((n = std::fread(buf, 1, sizeof buf, f)) > 0) text.append(buf, n);
-                const bool bad = std::ferror(f) != 0;
-                std::fclose(f);
-                if (bad) fail(GS_ERR_MODEL, "cannot read model file %s", r.model_path);
+            if (r.mode == GS_SEL_MODEL) {  // the other modes never consult a model
+                std::string text = kBuiltinModel;
+                if (r.model_path) {
+                    std::FILE *f = std::fopen(r.model_path, "rb");
+                    if (!f) fail(GS_ERR_MODEL, "cannot open model file %s", r.model_path);
+                    text.clear();
+                    char buf[1 << 16];
+                    size_t n;
+                    while ((n = std::fread(buf, 1, sizeof buf, f)) > 0) text.append(buf, n);
+                    const bool bad = std::ferror(f) != 0;
+                    std::fclose(f);
+                    if (bad) fail(GS_ERR_MODEL, "cannot read model file %s", r.model_path);
+                }
+                parse_model(text, c->model);
             }
-            parse_model(text, c->model);
         } catch (...) {
             delete c;
             throw;

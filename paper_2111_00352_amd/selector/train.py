@@ -131,16 +131,19 @@ def export(clf, mn, mx, path):
         base_scores = list(base)
     else:
         base_scores = [0.0, float(base[0])]
-    lines = ["GSMODEL 1", f"nfeat {mn.size}",
+    # version 2 of the model file: reals as exact hexadecimal literals,
+    # leaves as "L value", internal nodes as "feat thr left right"
+    hx = lambda v: float(v).hex()  # noqa: E731
+    lines = ["GSMODEL 2", f"nfeat {mn.size}",
              "classes %d %s" % (K, " ".join(str(FMT_IDS[TIE_ORDER[c]]) for c in classes)),
-             "min " + " ".join(repr(float(v)) for v in mn),
-             "max " + " ".join(repr(float(v)) for v in mx),
-             "base " + " ".join(repr(float(v)) for v in base_scores),
+             "min " + " ".join(hx(v) for v in mn),
+             "max " + " ".join(hx(v) for v in mx),
+             "base " + " ".join(hx(v) for v in base_scores),
              f"ntrees {len(trees)}"]
     for cls, nodes in trees:
         lines.append(f"tree {cls} {len(nodes)}")
         for f, thr, l, r, v in nodes:
-            lines.append(f"{f} {thr!r} {l} {r} {v!r}")
+            lines.append(f"L {hx(v)}" if f < 0 else f"{f} {hx(thr)} {l} {r}")
     with open(path, "w") as fh:
         fh.write("\n".join(lines) + "\n")
     return trees, base_scores, classes
@@ -159,21 +162,31 @@ def score_exported(trees, base_scores, Xn):
 
 
 def read_model(path):
-    """The exported model file: (min, max, base scores, class format ids,
-    trees), trees as written by ``export``."""
+    """The exported model file (version 1, decimal, or version 2, hexadecimal
+    reals): (min, max, base scores, class format ids, trees), trees as
+    written by ``export``."""
     with open(path) as fh:
         lines = [ln.split() for ln in fh if ln.strip()]
     head = {ln[0]: ln[1:] for ln in lines[:7]}
-    assert lines[0] == ["GSMODEL", "1"], "not a model file"
-    mn = np.array([float(v) for v in head["min"]])
-    mx = np.array([float(v) for v in head["max"]])
-    base = [float(v) for v in head["base"]]
+    assert lines[0] in (["GSMODEL", "1"], ["GSMODEL", "2"]), "not a model file"
+    real = float if lines[0][1] == "1" else float.fromhex
+
+    def node(tok):
+        if tok[0] == "L":
+            return (-1, 0.0, 0, 0, real(tok[1]))
+        if len(tok) == 4:
+            return (int(tok[0]), real(tok[1]), int(tok[2]), int(tok[3]), 0.0)
+        f, t, l, r, v = tok
+        return (int(f), real(t), int(l), int(r), real(v))
+
+    mn = np.array([real(v) for v in head["min"]])
+    mx = np.array([real(v) for v in head["max"]])
+    base = [real(v) for v in head["base"]]
     classes = [int(v) for v in head["classes"][1:]]
     trees, i = [], 7
     for _ in range(int(head["ntrees"][0])):
         _, cls, n = lines[i]
-        nodes = [(int(f), float(t), int(l), int(r), float(v)) for f, t, l, r, v in lines[i + 1:i + 1 + int(n)]]
-        trees.append((int(cls), nodes))
+        trees.append((int(cls), [node(t) for t in lines[i + 1:i + 1 + int(n)]]))
         i += 1 + int(n)
     return mn, mx, base, classes, trees
 

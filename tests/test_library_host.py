@@ -92,8 +92,29 @@ tree 1 3
 """
 
 
+# the same model in version 2: hexadecimal reals, "L value" leaves
+MODEL_OK_V2 = """GSMODEL 2
+nfeat 21
+classes 2 1 3
+min """ + " ".join(["0x0.0p+0"] * 21) + """
+max """ + " ".join(["0x1.0000000000000p+0"] * 21) + """
+base 0x1.0000000000000p-1 0x0.0p+0
+ntrees 1
+tree 1 3
+12 0x1.ccccccccccccdp-1 1 2
+L 0x0.0p+0
+L 0x1.0000000000000p+0
+"""
+
+
 @pytest.mark.parametrize("text,code", [
     (MODEL_OK, 0),
+    (MODEL_OK_V2, 0),
+    (MODEL_OK_V2.replace("0x1.ccccccccccccdp-1", "0.9"), gs.ERR_MODEL),            # decimal in version 2
+    (MODEL_OK_V2.replace("0x1.ccccccccccccdp-1", "0x1.ccgp-1"), gs.ERR_MODEL),     # not a hex digit
+    (MODEL_OK_V2.replace("0x1.ccccccccccccdp-1", "0x1.ccccccccccccdep-1"), gs.ERR_MODEL),  # 57 bits
+    (MODEL_OK_V2.replace("L 0x1.0000000000000p+0", "L"), gs.ERR_MODEL),            # leaf without value
+    (MODEL_OK_V2.replace("L 0x0.0p+0", "-1 0x0.0p+0 0 0"), gs.ERR_MODEL),         # leaf not marked
     ("", gs.ERR_MODEL),
     ("GSMODEL 2\n", gs.ERR_MODEL),
     (MODEL_OK.replace("nfeat 21", "nfeat 20"), gs.ERR_MODEL),
@@ -114,6 +135,11 @@ def test_model_file_parsing(L, tmp_path, text, code):
 def test_missing_model_file(L, tmp_path):
     rc, _ = _ctx(L, path=str(tmp_path / "absent.gsm").encode())
     assert rc == gs.ERR_MODEL
+    # the profiling and fixed selectors never read a model
+    for mode in (1, 2):
+        rc, h = _ctx(L, mode=mode, path=str(tmp_path / "absent.gsm").encode())
+        assert rc == 0, L.gs_last_error()
+        L.gs_ctx_destroy(h)
 
 
 def test_allocator_hooks_must_be_paired(L):
