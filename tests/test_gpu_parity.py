@@ -441,6 +441,40 @@ def test_buffers_return_to_the_hooks_that_allocated_them():
     check_spmm(case, case.build("csr"), graphgen.features_x(case.C, 8, 43, "normal"))
 
 
+def test_allocation_failure_is_reported_and_recovers():
+    # an allocator that returns NULL: the calls that need memory report
+    # GS_ERR_OOM and leave no half-made buffer behind, so once allocation
+    # works again the same handle builds its workspace and computes correctly
+    gs._require_gpu()
+    case = _random_case(3000, 2800, 60000, 71)
+    m = case.build("coo")
+    X = graphgen.features_x(case.C, 64, 72, "normal")
+    Xd = _dev(X)
+    refuse = {"on": True}
+
+    def _alloc(n, stream, _ctx):
+        if refuse["on"]:
+            return None
+        return torch.cuda.caching_allocator_alloc(int(n), stream=int(stream or 0))
+
+    def _free(p, _stream, _ctx):
+        torch.cuda.caching_allocator_delete(int(p))
+
+    hooks = gs._Allocator(gs._ALLOC_FN(_alloc), gs._FREE_FN(_free), None)
+    assert gs.lib().gs_set_allocator(ctypes.byref(hooks)) == 0
+    try:
+        for call in (lambda: m.spmm(Xd), lambda: case.build("csr")):  # COO ranges and carries; a whole build
+            with pytest.raises(gs.GnnSpmmError) as e:
+                call()
+            assert e.value.code == gs.ERR_OOM
+        refuse["on"] = False
+        check_spmm(case, m, X)
+        check_spmm(case, case.build("csr"), X)
+    finally:
+        gs._alloc_keep = None
+        gs._install_torch_allocator()
+
+
 def test_work_stays_on_the_callers_stream():
     # Everything on a second stream (default priority), queued behind an
     # asynchronous copy of X into a fresh buffer on that stream: builds,
