@@ -275,8 +275,11 @@ __global__ __launch_bounds__(kBlock) void k_plan_stats_final(const PlanStats *__
     if (threadIdx.x == 0) *st = p;
 }
 
+// Key of row i: its group (0 medium, 1 huge, 2 short) in the bits above the
+// rank, the rank (distance below the longest length, so longer rows first)
+// in the low `L` bits, so that the sort needs only L + 2 bits.
 __global__ __launch_bounds__(kBlock) void k_plan_keys(const int32_t *__restrict__ rp, int64_t R,
-                                                      int thr, int wg_thr, int sorted, int maxlen,
+                                                      int thr, int wg_thr, int sorted, int maxlen, int L,
                                                       uint64_t *__restrict__ keys)
 {
     for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < R;
@@ -284,20 +287,20 @@ __global__ __launch_bounds__(kBlock) void k_plan_keys(const int32_t *__restrict_
         const int len = rp[i + 1] - rp[i];
         const uint64_t group = len > thr ? (len > wg_thr ? 1u : 0u) : 2u;
         const uint32_t rank = group < 2 ? (uint32_t)(maxlen - len) : sorted ? (uint32_t)(thr - len) : 0u;
-        keys[i] = (group << 32) | rank;
+        keys[i] = (group << L) | rank;
     }
 }
 
 __global__ __launch_bounds__(kBlock) void k_plan_count(const int32_t *__restrict__ rp,
                                                        const uint64_t *__restrict__ keys,
                                                        const uint32_t *__restrict__ perm, int64_t R,
-                                                       int chunk, int32_t *__restrict__ cnt)
+                                                       int chunk, int L, int32_t *__restrict__ cnt)
 {
     for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < R;
          p += (int64_t)gridDim.x * kBlock) {
         const int64_t r = perm ? perm[p] : p;
         const int len = rp[r + 1] - rp[r];
-        cnt[p] = (keys[p] >> 32) < 2 ? (len + chunk - 1) / chunk : 1;
+        cnt[p] = (keys[p] >> L) < 2 ? (len + chunk - 1) / chunk : 1;
     }
 }
 
@@ -335,6 +338,17 @@ inline unsigned stats_grid(int64_t n)
 {
     int64_t g = ceil_div(n, (int64_t)kBlock * 4);
     return (unsigned)(g < 1 ? 1 : g > 2048 ? 2048 : g);
+}
+
+// The item counts at the three tier boundaries, gathered for one read-back.
+__global__ void k_pick3(const int32_t *__restrict__ cnt, int64_t a, int64_t b, int64_t c,
+                        int32_t *__restrict__ out)
+{
+    if (threadIdx.x == 0) {
+        out[0] = cnt[a];
+        out[1] = cnt[b];
+        out[2] = cnt[c];
+    }
 }
 
 }  // namespace
@@ -396,22 +410,25 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
         kb.alloc((size_t)R * 8, s);
         pa.alloc((size_t)R * 4, s);
         pb.alloc((size_t)R * 4, s);
-        k_plan_keys<<<plan_grid(R), kBlock, 0, s>>>(rp, R, thr, wg_thr_eff, sorted ? 1 : 0, st.maxlen,
+        // ranks are at most max(longest row, thr): L bits, the group above them
+        const int L = bits_for(std::max(st.maxlen, thr));
+        k_plan_keys<<<plan_grid(R), kBlock, 0, s>>>(rp, R, thr, wg_thr_eff, sorted ? 1 : 0, st.maxlen, L,
                                                     ka.as<uint64_t>());
         GS_HIP(hipGetLastError());
         std::vector<int> shifts;
-        for (int sft = 0; sft < bits_for(std::max(st.maxlen, thr)); sft += 8) shifts.push_back(sft);
-        shifts.push_back(32);
+        for (int sft = 0; sft < L + 2; sft += 8) shifts.push_back(sft);
         uint64_t *keys = nullptr;
         radix_sort_pairs(ka.as<uint64_t>(), kb.as<uint64_t>(), pa.as<uint32_t>(), pb.as<uint32_t>(), R,
                          shifts, s, &keys, &perm);
         cnt.alloc((size_t)(R + 1) * 4, s);
-        k_plan_count<<<plan_grid(R), kBlock, 0, s>>>(rp, keys, perm, R, chunk, cnt.as<int32_t>());
+        k_plan_count<<<plan_grid(R), kBlock, 0, s>>>(rp, keys, perm, R, chunk, L, cnt.as<int32_t>());
         GS_HIP(hipGetLastError());
         exclusive_scan_i32(cnt.as<int32_t>(), cnt.as<int32_t>(), R, true, s);
-        const int64_t at[3] = {m.n_medium_rows, n_long, R};
-        for (int i = 0; i < 3; i++)
-            GS_HIP(hipMemcpyAsync(&h_off[i], cnt.as<int32_t>() + at[i], 4, hipMemcpyDeviceToHost, s));
+        DevBuf picked;
+        picked.alloc(sizeof h_off, s);
+        k_pick3<<<1, kWave, 0, s>>>(cnt.as<int32_t>(), m.n_medium_rows, n_long, R, picked.as<int32_t>());
+        GS_HIP(hipGetLastError());
+        GS_HIP(hipMemcpyAsync(h_off, picked.p, sizeof h_off, hipMemcpyDeviceToHost, s));
         GS_HIP(hipStreamSynchronize(s));
     }
     m.n_medium_chunks = h_off[0];
