@@ -100,7 +100,9 @@ typedef struct gs_ctx_ *gs_ctx;       /* opaque; per-adjacency feature/format ca
 
 /* Installs the device allocator for all later allocations (NULL restores
  * hipMalloc/hipFree).  Memory always goes back through the hooks that
- * allocated it, so handles built before a change stay valid.  Not
+ * allocated it, so handles built before a change stay valid; hooks (and
+ * their ctx) must therefore remain callable until every handle and
+ * context that allocated through them has been destroyed.  Not
  * thread-safe against concurrent library calls. */
 int gs_set_allocator(const gs_allocator *a);
 

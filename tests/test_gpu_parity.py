@@ -462,15 +462,25 @@ def test_allocation_failure_is_reported_and_recovers():
 
     hooks = gs._Allocator(gs._ALLOC_FN(_alloc), gs._FREE_FN(_free), None)
     assert gs.lib().gs_set_allocator(ctypes.byref(hooks)) == 0
+    m2 = None
     try:
-        for call in (lambda: m.spmm(Xd), lambda: case.build("csr")):  # COO ranges and carries; a whole build
-            with pytest.raises(gs.GnnSpmmError) as e:
-                call()
-            assert e.value.code == gs.ERR_OOM
+        with pytest.raises(gs.GnnSpmmError) as e1:  # COO range bounds and carry slots
+            m.spmm(Xd)
+        with pytest.raises(gs.GnnSpmmError) as e2:  # a whole build
+            case.build("csr")
+        assert e1.value.code == gs.ERR_OOM and e2.value.code == gs.ERR_OOM
+        del e1, e2
         refuse["on"] = False
         check_spmm(case, m, X)
-        check_spmm(case, case.build("csr"), X)
+        m2 = case.build("csr")
+        check_spmm(case, m2, X)
     finally:
+        # buffers go back through the hooks that made them: every handle that
+        # allocated through these hooks is destroyed while they still exist
+        m.close()
+        if m2 is not None:
+            m2.close()
+        torch.cuda.synchronize()
         gs._alloc_keep = None
         gs._install_torch_allocator()
 
