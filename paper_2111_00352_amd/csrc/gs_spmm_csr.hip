@@ -300,7 +300,7 @@ __global__ __launch_bounds__(kBlock) void k_plan_count(const int32_t *__restrict
          p += (int64_t)gridDim.x * kBlock) {
         const int64_t r = perm ? perm[p] : p;
         const int len = rp[r + 1] - rp[r];
-        cnt[p] = (keys[p] >> L) < 2 ? (len + chunk - 1) / chunk : 1;
+        cnt[p] = keys && (keys[p] >> L) < 2 ? (len + chunk - 1) / chunk : 1;  // no keys: every row short
     }
 }
 
@@ -406,20 +406,22 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
     DevBuf ka, kb, pa, pb, cnt;
     uint32_t *perm = nullptr;
     if (R > 0) {
-        ka.alloc((size_t)R * 8, s);
-        kb.alloc((size_t)R * 8, s);
-        pa.alloc((size_t)R * 4, s);
-        pb.alloc((size_t)R * 4, s);
         // ranks are at most max(longest row, thr): L bits, the group above them
         const int L = bits_for(std::max(st.maxlen, thr));
-        k_plan_keys<<<plan_grid(R), kBlock, 0, s>>>(rp, R, thr, wg_thr_eff, sorted ? 1 : 0, st.maxlen, L,
-                                                    ka.as<uint64_t>());
-        GS_HIP(hipGetLastError());
-        std::vector<int> shifts;
-        for (int sft = 0; sft < L + 2; sft += 8) shifts.push_back(sft);
         uint64_t *keys = nullptr;
-        radix_sort_pairs(ka.as<uint64_t>(), kb.as<uint64_t>(), pa.as<uint32_t>(), pb.as<uint32_t>(), R,
-                         shifts, s, &keys, &perm);
+        if (sorted || n_long > 0) {  // otherwise every key is equal: natural order, no sort
+            ka.alloc((size_t)R * 8, s);
+            kb.alloc((size_t)R * 8, s);
+            pa.alloc((size_t)R * 4, s);
+            pb.alloc((size_t)R * 4, s);
+            k_plan_keys<<<plan_grid(R), kBlock, 0, s>>>(rp, R, thr, wg_thr_eff, sorted ? 1 : 0, st.maxlen, L,
+                                                        ka.as<uint64_t>());
+            GS_HIP(hipGetLastError());
+            std::vector<int> shifts;
+            for (int sft = 0; sft < L + 2; sft += 8) shifts.push_back(sft);
+            radix_sort_pairs(ka.as<uint64_t>(), kb.as<uint64_t>(), pa.as<uint32_t>(), pb.as<uint32_t>(), R,
+                             shifts, s, &keys, &perm);
+        }
         cnt.alloc((size_t)(R + 1) * 4, s);
         k_plan_count<<<plan_grid(R), kBlock, 0, s>>>(rp, keys, perm, R, chunk, L, cnt.as<int32_t>());
         GS_HIP(hipGetLastError());
