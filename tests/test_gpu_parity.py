@@ -432,8 +432,9 @@ def test_buffers_return_to_the_hooks_that_allocated_them():
         m = case.build("coo")
         check_spmm(case, m, graphgen.features_x(case.C, 64, 42, "normal"))
     finally:
-        gs._alloc_keep = None
-        gs._install_torch_allocator()
+        # the binding's own hooks, the same objects: buffers they allocated
+        # earlier must find them alive when freed
+        assert gs.lib().gs_set_allocator(ctypes.byref(gs._alloc_keep[0])) == 0
     assert live  # the handle holds its arrays and workspace
     m.close()
     torch.cuda.synchronize()
@@ -481,8 +482,9 @@ def test_allocation_failure_is_reported_and_recovers():
         if m2 is not None:
             m2.close()
         torch.cuda.synchronize()
-        gs._alloc_keep = None
-        gs._install_torch_allocator()
+        # the binding's own hooks, the same objects: buffers they allocated
+        # earlier must find them alive when freed
+        assert gs.lib().gs_set_allocator(ctypes.byref(gs._alloc_keep[0])) == 0
 
 
 def test_work_stays_on_the_callers_stream():
