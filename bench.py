@@ -1,19 +1,33 @@
 #!/usr/bin/env python3
 """SpMM benchmark: GNN aggregation Y = A.X with per-layer format selection.
 
-One step = one GNN layer's aggregation through the selector
-(gs_select_and_run) on one batch of features, with the adjacency's features,
-prediction and format conversion already cached from the warm-up (the paper
-decides the format once per layer across epochs, Sec. 5.2); those first-call
-costs are measured and reported separately.  Steps rotate over several
-(X, Y) batches so that consecutive steps do not find their operands in the
-256 MiB last-level cache.
+Headline workload: the large two-layer GNN forward.  A is a Chung-Lu
+power-law graph with n = 2,000,000 nodes (exponent 2.0, mean degree 25, about
+52M stored entries), with self-loops and row-stochastic fp32 values; the
+feature width is F = 128.  One step is that forward's two aggregations, each
+through the selector (gs_select_and_run):
+  layer 1: Y1 = A.X1, where X1 is n x 128 N(0,1);
+  layer 2: Y2 = A.X2, where X2 = ReLU((A.X1) W) with W 128 x 128 N(0, 1/128),
+           about half zeros, prepared before the timed region.
+The format is re-selected for layer 2 (Sec. 4.6: the decision is made per
+layer).  The adjacency's features, prediction and conversion come from the
+warm-up, as the paper decides once per layer across epochs (Sec. 5.2); these
+first-call costs are measured and reported separately.  Steps rotate over
+two input batches, so that no step finds its operands in the 256 MiB
+last-level cache.
 
-Headline workload: the power-law graph (n = 100,000, Chung-Lu exponent 2.1,
-mean degree 10, GCN-normalised fp32, X 100,000 x 128 fp32).  Also reported:
-every format's SpMM time on the same workload, the selector's speedup over
-fixed CSR, the roofline fraction of the dominant kernel, and the CPU oracle's
-throughput on this machine's cores.
+value = 2 layers x 2 nnz F flops / wall time per step (GFLOP/s).
+
+Also reported:
+  * per layer: the chosen format, the SpMM duration (HIP events on the stream
+    the kernels run on) and its fraction of the HBM roofline, against
+    B_alg = 4(R+1) + 8 nnz + 4 C F + 4 R F bytes;
+  * every feasible format's SpMM time on the headline workload and on the four
+    smaller workloads (tiny, power-law, mesh, block-community), with the
+    selector's choice and its speedup over fixed CSR;
+  * a 10-epoch two-layer GCN trained end to end with the selector and with
+    fixed CSR / COO;
+  * the CPU oracle's SpMM rate on this host's cores (bounded sample).
 """
 from __future__ import annotations
 
@@ -29,17 +43,22 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
+METRIC = "SpMM GFLOP/s (2*nnz*F) + % HBM roofline per format; best-vs-CSR speedup"
 
 WORKLOADS = {
     1: "tiny ER GCN n=2048 F=64",
     2: "power-law Chung-Lu n=100000 gamma=2.1 deg=10 GCN F=128",
     3: "mesh 512x512 5-point n=262144 F=64",
     4: "block-community n=204800 (16-node blocks p=0.8, 2 inter/node) GCN F=256",
-    5: "large Chung-Lu n=2000000 gamma=2.0 deg=25 row-stochastic F=128 (layer 1)",
+    5: "large 2-layer GNN forward: Chung-Lu n=2000000 gamma=2.0 deg=25 row-stochastic F=128, "
+       "layer 2 input ReLU((A X1) W), format re-selected per layer",
 }
-
-
 WORKLOAD_KEYS = {1: "tiny", 2: "powerlaw", 3: "mesh", 4: "blocks", 5: "large"}
+FORMAT_LIST = ("csr", "coo", "ell", "dia", "bsr", "csc")
+
+
+def log(msg: str):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 def b_alg(R, C, Z, F):
@@ -47,57 +66,115 @@ def b_alg(R, C, Z, F):
     return 4 * (R + 1) + 8 * Z + 4 * C * F + 4 * R * F
 
 
-def time_launches(fn, stream, reps, inputs):
-    """Per-launch durations (s) of fn(i) measured with HIP events on `stream`."""
+def event_durations(fns, stream, reps, inputs):
+    """Per-call durations (s) of each fn in fns, called in turn reps times on
+    rotating inputs and bracketed by HIP events recorded on `stream` (the
+    stream the library launches on).  Returns one array per fn."""
     import torch
 
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)] for _ in range(reps)]
     for i in range(reps):
         ev[i][0].record(stream)
-        fn(inputs[i % len(inputs)])
-        ev[i][1].record(stream)
+        for j, fn in enumerate(fns):
+            fn(inputs[i % len(inputs)])
+            ev[i][j + 1].record(stream)
     torch.cuda.synchronize()
-    return np.array([a.elapsed_time(b) * 1e-3 for a, b in ev])
+    return [np.array([ev[i][j].elapsed_time(ev[i][j + 1]) * 1e-3 for i in range(reps)])
+            for j in range(len(fns))]
 
 
-def cpu_baseline(g, F, budget_s=10.0):
-    """The oracle's SpMM on this host: all threads for about budget_s, then
-    one thread for a quarter of that (the results are identical)."""
+def adaptive_reps(t_once: float, want: int, budget_s: float = 1.0) -> int:
+    return int(max(3, min(want, budget_s / max(t_once, 1e-7))))
+
+
+def stats_row(d, flops, balg):
+    t, tm = float(np.median(d)), float(np.mean(d))
+    return {"median_us": round(t * 1e6, 2), "mean_us": round(tm * 1e6, 2),
+            "min_us": round(float(d.min()) * 1e6, 2), "p90_us": round(float(np.percentile(d, 90)) * 1e6, 2),
+            "reps": int(d.size), "gflops": round(flops / t / 1e9, 1),
+            "roofline_frac": round(balg / t / 1e9 / HBM_PEAK_GBS, 4)}
+
+
+def format_table(gs, row, col, val, shape, pairs, stream, reps, flops, balg):
+    """Median SpMM time of every feasible format on rotating (X, Y) pairs."""
+    import torch
+
+    R, C = shape
+    out = {}
+    for fmt in FORMAT_LIST:
+        try:
+            t0 = time.perf_counter()
+            m = gs.build_format(row, col, val, (R, C), fmt)
+            torch.cuda.synchronize()
+            t_build = time.perf_counter() - t0
+        except gs.GnnSpmmError as e:
+            out[fmt] = {"feasible": False, "bytes_required": getattr(e, "bytes_required", None)}
+            continue
+        for i in range(2):
+            m.spmm(pairs[i % len(pairs)][0], out=pairs[i % len(pairs)][1])
+        (d1,) = event_durations([lambda p: m.spmm(p[0], out=p[1])], stream, 1, pairs)
+        n = adaptive_reps(float(d1[0]), reps)
+        (d,) = event_durations([lambda p: m.spmm(p[0], out=p[1])], stream, n, pairs)
+        out[fmt] = {"feasible": True, **stats_row(d, flops, balg), "format_bytes": m.device_bytes,
+                    "build_s": round(t_build, 4)}
+        m.close()
+        del m
+    return out
+
+
+def selector_summary(fmts, chosen):
+    feasible = {k: v for k, v in fmts.items() if v.get("feasible")}
+    best = min(feasible, key=lambda k: feasible[k]["median_us"])
+    t_csr, t_ch, t_best = (feasible[k]["median_us"] for k in ("csr", chosen, best))
+    return {"chosen": chosen, "best_measured": best,
+            "speedup_vs_csr": round(t_csr / t_ch, 3), "best_vs_csr": round(t_csr / t_best, 3),
+            "fraction_of_best": round(t_best / t_ch, 3),
+            "speedup_vs_coo": round(feasible["coo"]["median_us"] / t_ch, 3),
+            "best_roofline_frac": feasible[best]["roofline_frac"]}
+
+
+def cpu_baseline(g, F, budget_s=10.0, sample_rows=100_000):
+    """The oracle's SpMM on this host: the whole matrix on all threads for
+    about budget_s, then the first sample_rows rows on one thread for a
+    quarter of that (each row's result is the same for any thread count)."""
     import oracle
 
     rp = oracle.csr(g.R, g.row)
-    X = g.X[:, :F]
+    X = np.ascontiguousarray(g.X[:, :F])
 
-    def rate(budget):
+    def rate(R, budget):
+        nnz = int(rp[R])
         t0 = time.perf_counter()
         reps = 0
         while True:
-            oracle.spmm(g.R, rp, g.col, g.val, X)
+            oracle.spmm(R, rp[:R + 1], g.col[:nnz], g.val[:nnz], X)
             reps += 1
             el = time.perf_counter() - t0
             if el >= budget:
-                return 2.0 * g.nnz * F * reps / el / 1e9, reps, el
+                return 2.0 * nnz * F * reps / el / 1e9, reps, el
 
     threads = oracle.num_threads()
-    v, reps, el = rate(budget_s)
+    v, reps, el = rate(g.R, budget_s)
     oracle.set_threads(1)
-    v1, reps1, el1 = rate(budget_s / 4)
+    R1 = min(g.R, sample_rows)
+    v1, reps1, el1 = rate(R1, budget_s / 4)
     oracle.set_threads(threads)
     return {
         "value": round(v, 3),
         "unit": "GFLOP/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": f"full {g.R}-row SpMM (fp64 accumulation, plus |A||X|) repeated {reps}x in {el:.1f}s "
-                  f"on {threads} threads; single thread: {reps1}x in {el1:.1f}s",
+        "sample": f"whole {g.R}-row, {g.nnz}-entry layer-1 SpMM (fp64 accumulation plus |A||X|) "
+                  f"repeated {reps}x in {el:.1f}s on {threads} threads; single thread: its first "
+                  f"{R1} rows {reps1}x in {el1:.1f}s",
         "single_thread_value": round(v1, 3),
     }
 
 
-def gcn_e2e(g, row, col, val, X, args, hidden=128, out_dim=64):
-    """Two-layer GCN trained for 10 epochs (Sec. 5.2) with the selector and with
-    fixed CSR / COO, each from a fresh context so every first-call cost is
-    inside its total."""
+def gcn_e2e(g, row, col, val, X, epochs, hidden=128, out_dim=64):
+    """Two-layer GCN trained for `epochs` epochs (Sec. 5.2) with the selector
+    and with fixed CSR / COO, each from a fresh context so every first-call
+    cost is inside its total."""
     import torch
 
     import graphgen
@@ -109,9 +186,9 @@ def gcn_e2e(g, row, col, val, X, args, hidden=128, out_dim=64):
     W1 = torch.from_numpy(graphgen.features_x(F, hidden, 4100, "normal")).to(dev) / F ** 0.5
     W2 = torch.from_numpy(graphgen.features_x(hidden, out_dim, 4200, "normal")).to(dev) / hidden ** 0.5
     T = torch.from_numpy(graphgen.features_x(g.R, out_dim, 4300, "normal")).to(dev)
-    res = gcn.end_to_end(row, col, val, (g.R, g.C), X, T, W1, W2, epochs=args.gcn_epochs, lr=0.1,
+    res = gcn.end_to_end(row, col, val, (g.R, g.C), X, T, W1, W2, epochs=epochs, lr=0.1,
                          symmetric=bool(g.meta.get("symmetric", False)))
-    r = {"epochs": args.gcn_epochs, "hidden": hidden, "out": out_dim}
+    r = {"epochs": epochs, "hidden": hidden, "out": out_dim}
     for k, v in res.items():
         if isinstance(v, dict):
             r[k] = {"total_ms": round(v["total_s"] * 1e3, 3), "first_epoch_ms": round(v["first_epoch_s"] * 1e3, 3),
@@ -122,24 +199,68 @@ def gcn_e2e(g, row, col, val, X, args, hidden=128, out_dim=64):
     return r
 
 
+def library_warmup(gs, dev, F):
+    """One-time library start-up (code objects loaded on first launch), paid
+    once per process, not per matrix: taken on a small identity matrix."""
+    import torch
+
+    t0 = time.perf_counter()
+    n0 = 256
+    i0 = torch.arange(n0, dtype=torch.int32, device=dev)
+    warm = gs.SelectContext("model")
+    for fmt in FORMAT_LIST:
+        gs.build_format(i0, i0, torch.ones(n0, device=dev), (n0, n0), fmt).spmm(torch.ones((n0, F), device=dev))
+    warm.run(0, i0, i0, torch.ones(n0, device=dev), (n0, n0), torch.ones((n0, F), device=dev))
+    torch.cuda.synchronize()
+    warm.close()
+    return time.perf_counter() - t0
+
+
+def other_workload(gs, k, dev, stream, reps):
+    """Per-format table and selector choice on workload k (one layer)."""
+    import torch
+
+    import graphgen
+
+    g = graphgen.config(k)
+    R, C, Z, F = g.R, g.C, g.nnz, g.F
+    row, col, val = (torch.from_numpy(a).to(dev) for a in (g.row, g.col, g.val))
+    rng = np.random.default_rng(7)
+    pairs = []
+    for b in range(4):
+        X = torch.from_numpy(g.X if b == 0 else rng.permutation(g.X, axis=0)).to(dev)
+        pairs.append((X, torch.empty((R, F), dtype=torch.float32, device=dev)))
+    flops, balg = 2.0 * Z * F, b_alg(R, C, Z, F)
+    fmts = format_table(gs, row, col, val, (R, C), pairs, stream, reps, flops, balg)
+    ctx = gs.SelectContext("model")
+    _, chosen = ctx.run(1, row, col, val, (R, C), pairs[0][0], out=pairs[0][1])
+    torch.cuda.synchronize()
+    ctx.close()
+    return {"workload": WORKLOADS[k], "n": R, "nnz": Z, "F": F, "B_alg": balg,
+            "selector": selector_summary(fmts, chosen), "formats": fmts}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default: power-law)")
-    ap.add_argument("--batches", type=int, default=4, help="rotating (X, Y) batches")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=5,
+                    help="headline workload 1..5 (default 5, the two-layer 2M-node forward)")
+    ap.add_argument("--batches", type=int, default=2, help="rotating input batches")
+    ap.add_argument("--others", default="1,2,3,4",
+                    help="further workloads whose per-format tables are reported ('' for none)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
-    ap.add_argument("--format-reps", type=int, default=50)
+    ap.add_argument("--format-reps", type=int, default=20)
     ap.add_argument("--no-gcn", action="store_true", help="skip the two-layer GCN end-to-end run")
     ap.add_argument("--gcn-epochs", type=int, default=10)
     ap.add_argument("--profile-run", action="store_true",
-                    help="only run the timed steps plus a 256 MiB calibration copy (for rocprofv3)")
+                    help="only the warm-up and timed steps plus a 256 MiB calibration copy (for rocprofv3)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: runs on one GPU only (there is no multi-GPU path); use --gpus 1",
+        print("bench.py: this build runs on one GPU only (it has no multi-GPU path); use --gpus 1",
               file=sys.stderr)
         sys.exit(2)
 
@@ -150,51 +271,70 @@ def main():
 
     assert torch.cuda.is_available(), "bench needs a GPU"
     torch.cuda.set_device(0)
+    torch.backends.cuda.matmul.allow_tf32 = False
     dev = torch.device("cuda", 0)
     stream = torch.cuda.current_stream()
+    k = args.config
+    two_layer = k == 5
 
     t_gen = time.perf_counter()
-    g = graphgen.config(args.config)
+    g = graphgen.config(k)
     t_gen = time.perf_counter() - t_gen
+    log(f"generated {WORKLOAD_KEYS[k]}: n={g.R} nnz={g.nnz} F={g.F} in {t_gen:.1f}s")
     R, C, Z, F = g.R, g.C, g.nnz, g.F
-    row = torch.from_numpy(g.row).to(dev)
-    col = torch.from_numpy(g.col).to(dev)
-    val = torch.from_numpy(g.val).to(dev)
-    Xs, Ys = [], []
-    rng = np.random.default_rng(7)
-    for b in range(args.batches):
-        X = torch.from_numpy(g.X if b == 0 else rng.permutation(g.X, axis=0)).to(dev)
-        Xs.append(X)
-        Ys.append(torch.empty((R, F), dtype=torch.float32, device=dev))
-    torch.cuda.synchronize()
+    row, col, val = (torch.from_numpy(a).to(dev) for a in (g.row, g.col, g.val))
+    X0 = torch.from_numpy(g.X).to(dev)
+    flops1, balg1 = 2.0 * Z * F, b_alg(R, C, Z, F)
+    n_layers = 2 if two_layer else 1
 
-    flops = 2.0 * Z * F
-    balg = b_alg(R, C, Z, F)
+    library_init_s = library_warmup(gs, dev, F)
 
-    # ---- one-time library start-up (code objects loaded on first launch),
-    # paid once per process, not per matrix: taken on a small identity matrix
-    t0 = time.perf_counter()
-    n0 = 256
-    i0 = torch.arange(n0, dtype=torch.int32, device=dev)
-    warm = gs.SelectContext("model")
-    for fmt_probe in ("csr", "coo", "ell", "dia", "bsr", "csc"):
-        gs.build_format(i0, i0, torch.ones(n0, device=dev), (n0, n0), fmt_probe).spmm(
-            torch.ones((n0, F), device=dev))
-    warm.run(0, i0, i0, torch.ones(n0, device=dev), (n0, n0), torch.ones((n0, F), device=dev))
-    torch.cuda.synchronize()
-    warm.close()
-    library_init_s = time.perf_counter() - t0
-
-    # ---- selector: first call (features + prediction + conversion), then steady state
+    # ---- selector, layer 1: first call (features + prediction + conversion)
     ctx = gs.SelectContext("model")
+    Y0 = torch.empty((R, F), dtype=torch.float32, device=dev)
     t0 = time.perf_counter()
-    _, chosen = ctx.run(1, row, col, val, (R, C), Xs[0], out=Ys[0])
+    _, chosen1 = ctx.run(1, row, col, val, (R, C), X0, out=Y0)
     torch.cuda.synchronize()
     first_call_s = time.perf_counter() - t0
-    st = ctx.stats()
+    st1 = ctx.stats()
+
+    # ---- inputs: batch b permutes X's rows (a fresh operand for the cache);
+    # the layer-2 input is ReLU((A X1) W), computed here through the library
+    batches = []
+    W = torch.from_numpy(graphgen.layer2_weight(F)).to(dev) if two_layer else None
+    gen = torch.Generator(device="cpu").manual_seed(7)
+    for b in range(args.batches):
+        X1 = X0 if b == 0 else X0[torch.randperm(C, generator=gen).to(dev)]
+        Y1 = torch.empty((R, F), dtype=torch.float32, device=dev)
+        if two_layer:
+            ctx.run(1, row, col, val, (R, C), X1, out=Y1)
+            X2 = torch.relu(Y1 @ W).contiguous()
+            batches.append((X1, Y1, X2, torch.empty((R, F), dtype=torch.float32, device=dev)))
+        else:
+            batches.append((X1, Y1))
+    torch.cuda.synchronize()
+    zero_frac2 = None
+    chosen2 = None
+    first_call2_s = None
+    if two_layer:
+        zero_frac2 = float((batches[0][2] == 0).float().mean().item())
+        t0 = time.perf_counter()
+        _, chosen2 = ctx.run(1, row, col, val, (R, C), batches[0][2], out=batches[0][3])
+        torch.cuda.synchronize()
+        first_call2_s = time.perf_counter() - t0
+    log(f"selector: layer 1 -> {chosen1}" + (f", layer 2 -> {chosen2}" if two_layer else ""))
+
+    def layer1(bt):
+        return ctx.run(1, row, col, val, (R, C), bt[0], out=bt[1])
+
+    def layer2(bt):
+        return ctx.run(1, row, col, val, (R, C), bt[2], out=bt[3])
 
     def step(i):
-        return ctx.run(1, row, col, val, (R, C), Xs[i % args.batches], out=Ys[i % args.batches])
+        bt = batches[i % len(batches)]
+        layer1(bt)
+        if two_layer:
+            layer2(bt)
 
     for i in range(args.warmup):
         step(i)
@@ -205,56 +345,54 @@ def main():
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
     ms_per_step = el / args.steps * 1e3
-    value = flops / (el / args.steps) / 1e9
+    value = n_layers * flops1 / (el / args.steps) / 1e9
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {value:.1f} GFLOP/s")
     if args.profile_run:
         # plain elementwise copy of known size: calibrates the byte counters
         src = torch.ones(64 * 2**20, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
         torch.neg(src, out=dst)
         torch.cuda.synchronize()
-        print(f"profile run: {args.steps} steps of spmm_{chosen}, {ms_per_step * 1e3:.2f} us/step", flush=True)
+        print(f"profile run: {args.steps} steps, {ms_per_step * 1e3:.2f} us/step "
+              f"(layer formats {chosen1}{', ' + chosen2 if two_layer else ''})", flush=True)
         return
 
-    # ---- per-launch duration of the chosen format's SpMM (HIP events on its stream)
-    mats = {}
-    fmt_rows = {}
-    for fmt in ("csr", "coo", "ell", "dia", "bsr", "csc"):
-        try:
-            t0 = time.perf_counter()
-            m = gs.build_format(row, col, val, (R, C), fmt)
-            torch.cuda.synchronize()
-            t_build = time.perf_counter() - t0
-        except gs.GnnSpmmError as e:
-            fmt_rows[fmt] = {"feasible": False, "bytes_required": getattr(e, "bytes_required", None)}
-            continue
-        mats[fmt] = m
-        pairs = list(zip(Xs, Ys))
-        for i in range(3):
-            m.spmm(*pairs[i % len(pairs)][:1], out=pairs[i % len(pairs)][1])
-        d = time_launches(lambda p: m.spmm(p[0], out=p[1]), stream, args.format_reps, pairs)
-        t = float(np.median(d))
-        fmt_rows[fmt] = {
-            "feasible": True, "median_us": round(t * 1e6, 2), "min_us": round(float(d.min()) * 1e6, 2),
-            "p90_us": round(float(np.percentile(d, 90)) * 1e6, 2),
-            "gflops": round(flops / t / 1e9, 1), "roofline_frac": round(balg / t / 1e9 / HBM_PEAK_GBS, 4),
-            "format_bytes": m.device_bytes, "build_s": round(t_build, 4),
-        }
-    d_sel = time_launches(lambda p: ctx.run(1, row, col, val, (R, C), p[0], out=p[1]), stream,
-                          args.format_reps, list(zip(Xs, Ys)))
-    t_sel = float(np.median(d_sel))
-    feasible = {k: v for k, v in fmt_rows.items() if v.get("feasible")}
-    best = min(feasible, key=lambda k: feasible[k]["median_us"])
-    t_csr = feasible["csr"]["median_us"]
-    achieved = balg / t_sel / 1e9
-    # amortised over 10 epochs of one layer (Sec. 5.2): the selector pays its
-    # first call (features, prediction, conversion, one SpMM) once; fixed CSR
+    # ---- per-layer SpMM duration through the selector (HIP events on its stream)
+    fns = [layer1, layer2] if two_layer else [layer1]
+    durs = event_durations(fns, stream, max(args.format_reps, 20), batches)
+    layers = []
+    for li, (d, ch) in enumerate(zip(durs, [chosen1, chosen2][:n_layers])):
+        tm = float(np.mean(d))
+        layers.append({"layer": li + 1, "chosen": ch, **stats_row(d, flops1, balg1),
+                       "achieved_gbs": round(balg1 / tm / 1e9, 1)})
+    log("per-layer: " + ", ".join(f"L{x['layer']} {x['chosen']} {x['mean_us']} us" for x in layers))
+
+    # ---- every feasible format on this workload (layer-1 operands)
+    pairs = [(bt[0], bt[1]) for bt in batches]
+    fmts = format_table(gs, row, col, val, (R, C), pairs, stream, args.format_reps, flops1, balg1)
+    sel1 = selector_summary(fmts, chosen1)
+    log("formats: " + ", ".join(f"{f} {v.get('median_us', 'n/a')}" for f, v in fmts.items()))
+    fmts2 = None
+    if two_layer:
+        pairs2 = [(bt[2], bt[3]) for bt in batches]
+        fmts2 = format_table(gs, row, col, val, (R, C), pairs2, stream, args.format_reps, flops1, balg1)
+    t_csr = fmts["csr"]["median_us"] * 1e-6
+    t_csr2 = fmts2["csr"]["median_us"] * 1e-6 if two_layer else 0.0
+    t_sel = sum(float(np.median(d)) for d in durs)
+    # amortised over 10 epochs (Sec. 5.2): the selector pays its first calls
+    # (features, prediction, conversion, one SpMM per layer) once; fixed CSR
     # pays its build once
     epochs = 10
-    e2e_sel = first_call_s + (epochs - 1) * t_sel
-    e2e_csr = feasible["csr"]["build_s"] + epochs * feasible["csr"]["median_us"] * 1e-6
+    first_total = first_call_s + (first_call2_s or 0.0)
+    e2e_sel = first_total + (epochs - 1) * t_sel
+    e2e_csr = fmts["csr"]["build_s"] + epochs * (t_csr + t_csr2)
 
+    # ---- roofline of the dominant kernel: the layer-1 SpMM (the layers are
+    # the same matrix and width); the time is the mean launch duration
+    dom = layers[0]
+    achieved = dom["achieved_gbs"]
     traffic = None
-    tpath = os.path.join(ROOT, "profiles", f"traffic_{WORKLOAD_KEYS[args.config]}_{chosen}.json")
+    tpath = os.path.join(ROOT, "profiles", f"traffic_{WORKLOAD_KEYS[k]}_{chosen1}.json")
     if os.path.exists(tpath):
         from paper_2111_00352_amd.profsum import source_hash
 
@@ -264,7 +402,7 @@ def main():
             traffic = round(tj["bytes"] / 1e6, 2)
 
     out = {
-        "metric": "SpMM GFLOP/s (2*nnz*F) + % HBM roofline per format; best-vs-CSR speedup",
+        "metric": METRIC,
         "value": round(value, 2),
         "unit": "GFLOP/s",
         "n_gpus": 1,
@@ -276,52 +414,63 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": WORKLOADS[args.config], "n": R, "nnz": Z, "F": F,
-                   "batches": args.batches},
+        "config": {"workload": WORKLOADS[k], "n": R, "nnz": Z, "F": F, "layers": n_layers,
+                   "batches": args.batches, "flops_per_step": n_layers * flops1},
         "roofline": {
             "bound": "hbm",
-            "kernel": f"spmm_{chosen} (all launches of one SpMM)",
-            "achieved": round(achieved, 1),
+            "kernel": f"spmm_{chosen1}, layer 1 (all launches of one SpMM)",
+            "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            # measured bytes over the same launch time: the rate the memory
-            # system actually sustains for this kernel
-            "traffic_rate_gbs": None if traffic is None else round(traffic * 1e6 / t_sel / 1e9, 1),
             "traffic_unit": "MB per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-            "bytes_per_launch": balg,
-            "launch_us": round(t_sel * 1e6, 2),
+            "traffic_rate_gbs": None if traffic is None else round(traffic * 1e6 / (dom["mean_us"] * 1e-6) / 1e9, 1),
+            "bytes_per_launch": balg1,
+            "launch_us": dom["mean_us"],
+            "layers": layers,
         },
         "selector": {
             "mode": "model",
-            "chosen": chosen,
-            "best_measured": best,
-            # steady-state kernel speedup of the chosen format over fixed CSR,
-            # and of the best measured format (the exhaustive-search reference)
-            "speedup_vs_csr": round(t_csr / feasible[chosen]["median_us"], 3),
-            "best_vs_csr": round(t_csr / feasible[best]["median_us"], 3),
-            "fraction_of_best": round(feasible[best]["median_us"] / feasible[chosen]["median_us"], 3),
-            "speedup_vs_coo": round(feasible["coo"]["median_us"] / feasible[chosen]["median_us"], 3),
+            "layer1": sel1,
+            "layer2": selector_summary(fmts2, chosen2) if two_layer else None,
+            "layer2_input_zero_fraction": None if zero_frac2 is None else round(zero_frac2, 4),
             "amortised_speedup_vs_csr_10_epochs": round(e2e_csr / e2e_sel, 3),
             "selector_step_us": round(t_sel * 1e6, 2),
-            "host_overhead_us": round(t_sel * 1e6 - feasible[chosen]["median_us"], 2),
             "first_call_s": round(first_call_s, 4),
+            "first_call_layer2_s": None if first_call2_s is None else round(first_call2_s, 5),
             "library_init_s": round(library_init_s, 4),
-            "t_features_s": round(st["t_features"], 4),
-            "t_predict_us": round(st["t_predict"] * 1e6, 2),
-            "t_convert_s": round(st["t_convert"], 4),
+            "t_features_s": round(st1["t_features"], 4),
+            "t_predict_us": round(st1["t_predict"] * 1e6, 2),
+            "t_convert_s": round(st1["t_convert"], 4),
         },
-        "formats": fmt_rows,
+        "formats": fmts,
+        "formats_layer2": fmts2,
         "gen_s": round(t_gen, 2),
         "device": torch.cuda.get_device_name(0),
         "arch": getattr(torch.cuda.get_device_properties(0), "gcnArchName", None),
         "compute_units": torch.cuda.get_device_properties(0).multi_processor_count,
         "hip": torch.version.hip,
     }
+    ctx.close()
+    del batches, pairs, Y0
+    torch.cuda.empty_cache()
     if not args.no_gcn:
-        out["gcn_e2e"] = gcn_e2e(g, row, col, val, Xs[0], args)
+        log("gcn end to end")
+        out["gcn_e2e"] = gcn_e2e(g, row, col, val, X0, args.gcn_epochs)
+    del X0, row, col, val
+    torch.cuda.empty_cache()
+    others = {}
+    for kk in [int(x) for x in args.others.split(",") if x.strip()]:
+        if kk == k:
+            continue
+        log(f"workload {WORKLOAD_KEYS[kk]}")
+        others[WORKLOAD_KEYS[kk]] = other_workload(gs, kk, dev, stream, args.format_reps)
+        torch.cuda.empty_cache()
+    if others:
+        out["other_workloads"] = others
     if not args.no_cpu:
+        log("cpu baseline")
         out["cpu_baseline"] = cpu_baseline(g, F, args.cpu_budget)
     print(json.dumps(out), flush=True)
 
