@@ -152,6 +152,27 @@ int gs_convert(gs_matrix A, int fmt, const gs_build_opts *opts, gs_stream s, gs_
 int gs_spmm(gs_matrix A, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
             gs_stream s);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): gs_spmm
+ * with the same arguments and the same result, bit for bit, that never calls
+ * the allocator.  The F-dependent workspace that gs_spmm keeps in the handle
+ * (partial sums of split CSR rows, the CSC fp64 accumulator) comes instead
+ * from a fixed array of GS_NOALLOC_SCRATCH_BYTES in device memory, one per
+ * device, reserved when the library's code is loaded on that device and held
+ * until the process ends.  Every call on one device shares that device's
+ * array and leaves it in an undefined state: calls that may overlap in time
+ * on one device (other streams, other threads) race, so order them.
+ * Supported for CSR, ELL, DIA, BSR and CSC handles built by gs_build_format
+ * or gs_convert.  Errors: GS_ERR_UNSUPPORTED for a COO handle (its range
+ * tables are built, and allocated, per launch shape on first use) and when
+ * the workspace would exceed GS_NOALLOC_SCRATCH_BYTES (CSR: 4 * F bytes per
+ * 128-entry chunk of rows longer than 1,024 entries, or longer than 128 when
+ * F is not a multiple of 4 or an operand is not 16-byte aligned; CSC:
+ * 8 * n_rows * F bytes); otherwise as gs_spmm.  Asynchronous on s. */
+#define GS_NOALLOC_SCRATCH_BYTES (64u << 20)
+int gs_spmm_noalloc(gs_matrix A, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+                    gs_stream s);
+
 /* Writes the canonical COO of A (sorted by (row, col)) into caller-allocated
  * [dev] arrays of nnz entries each.  For padded formats, padding slots are
  * dropped (ELL col == -1; DIA/BSR value == 0 or outside the matrix).

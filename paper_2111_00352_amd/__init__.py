@@ -115,6 +115,7 @@ def lib() -> ctypes.CDLL:
         "gs_build_format": (c_int, [P(_Coo), c_int, P(_BuildOpts), _p, P(_p), P(_u64)]),
         "gs_convert": (c_int, [_p, c_int, P(_BuildOpts), _p, P(_p), P(_u64)]),
         "gs_spmm": (c_int, [_p, _p, _i64, _p, _i64, _i64, _p]),
+        "gs_spmm_noalloc": (c_int, [_p, _p, _i64, _p, _i64, _i64, _p]),
         "gs_to_coo": (c_int, [_p, _p, _p, _p, _p]),
         "gs_get_info": (c_int, [_p, P(_Info)]),
         "gs_get_array": (c_int, [_p, c_int, P(_p), P(_u64)]),
@@ -241,6 +242,19 @@ class Matrix:
             raise ValueError("out has the wrong shape")
         _check(lib().gs_spmm(self._h, _ptr(X), X.stride(0), _ptr(out), out.stride(0), F,
                              _stream(stream)))
+        return out
+
+    def spmm_noalloc(self, X: torch.Tensor, out: torch.Tensor, stream=None) -> torch.Tensor:
+        """Y = A.X into the preallocated `out` without any device allocation
+        (gs_spmm_noalloc: the workspace is the library's fixed per-device
+        scratch array, shared by every such call on the device)."""
+        _check_dense(X, "X")
+        _check_dense(out, "out")
+        R, C = self.shape
+        if X.shape[0] != C or out.shape[0] != R or out.shape[1] != X.shape[1]:
+            raise ValueError("X / out shapes do not match A")
+        _check(lib().gs_spmm_noalloc(self._h, _ptr(X), X.stride(0), _ptr(out), out.stride(0), X.shape[1],
+                                     _stream(stream)))
         return out
 
     def to_coo(self, stream=None):

@@ -64,16 +64,16 @@ gs_matrix_ *build_csr(const gs_coo *A, const gs_build_opts &o, hipStream_t s, bo
 }
 
 void run_spmm(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
-              hipStream_t s)
+              hipStream_t s, const WorkArea *fixed)
 {
     if (m.R == 0) return;
     switch (m.fmt) {
-    case GS_CSR: spmm_csr(m, X, ldx, Y, ldy, F, s); break;
-    case GS_COO: spmm_coo(m, X, ldx, Y, ldy, F, s); break;
+    case GS_CSR: spmm_csr(m, X, ldx, Y, ldy, F, s, fixed); break;
+    case GS_COO: spmm_coo(m, X, ldx, Y, ldy, F, s, fixed); break;
     case GS_ELL: spmm_ell(m, X, ldx, Y, ldy, F, s); break;
     case GS_DIA: spmm_dia(m, X, ldx, Y, ldy, F, s); break;
     case GS_BSR: spmm_bsr(m, X, ldx, Y, ldy, F, s); break;
-    case GS_CSC: spmm_csc(m, X, ldx, Y, ldy, F, s); break;
+    case GS_CSC: spmm_csc(m, X, ldx, Y, ldy, F, s, fixed); break;
     default: fail(GS_ERR_INVALID_ARG, "corrupt matrix handle");
     }
 }

@@ -89,6 +89,8 @@ struct DevBuf {
     template <class T> T *as() const { return static_cast<T *>(p); }
 };
 
+struct WorkArea;
+
 // ------------------------------------------------------------ matrix handle
 
 }  // namespace gs
@@ -240,9 +242,9 @@ void diag_bitmap(const int32_t *rp, const int32_t *col, int64_t R, int64_t C, in
 // ------------------------------------------------------- spmm (gs_spmm_*)
 
 void spmm_csr(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
-              hipStream_t s);
+              hipStream_t s, const WorkArea *fixed = nullptr);
 void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
-              hipStream_t s);
+              hipStream_t s, const WorkArea *fixed = nullptr);
 void spmm_ell(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
               hipStream_t s);
 void spmm_dia(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
@@ -250,7 +252,7 @@ void spmm_dia(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
 void spmm_bsr(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
               hipStream_t s);
 void spmm_csc(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
-              hipStream_t s);
+              hipStream_t s, const WorkArea *fixed = nullptr);
 
 // Plans built at conversion time for the CSR and COO kernels.
 void plan_csr(gs_matrix_ &m, hipStream_t s);
@@ -258,7 +260,7 @@ void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s);
 
 // Vectorised CSR path; returns false when F / alignment do not allow it.
 bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
-                   hipStream_t s);
+                   hipStream_t s, const WorkArea *fixed = nullptr);
 
 // Workgroups of 256 threads the device keeps resident at full occupancy
 // (compute units x 8), queried once.
@@ -279,5 +281,25 @@ bool spmm_bsr16_mfma(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64
 
 // Makes sure m.work holds at least bytes (reallocating in stream order).
 void ensure_work(gs_matrix_ &m, size_t bytes, hipStream_t s);
+
+// Where an SpMM call takes its F-dependent workspace (partial sums of split
+// rows, the CSC accumulator): the handle's own buffer, grown through the
+// allocator on demand (fixed == nullptr), or a fixed buffer of cap bytes that
+// is never grown.
+struct WorkArea {
+    void *p = nullptr;
+    size_t cap = 0;
+};
+
+// A workspace of at least `bytes` for an SpMM on m: fixed->p when fixed is
+// given (GS_ERR_UNSUPPORTED when bytes exceed fixed->cap), else m.work grown
+// in stream order.
+void *work_for(gs_matrix_ &m, const WorkArea *fixed, size_t bytes, hipStream_t s);
+
+// Argument checks of gs_spmm (throws Error) and the format dispatch.
+void check_spmm_args(const gs_matrix_ *A, const float *X, int64_t ldx, const float *Y, int64_t ldy,
+                     int64_t F);
+void run_spmm(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
+              hipStream_t s, const WorkArea *fixed = nullptr);
 
 }  // namespace gs

@@ -77,6 +77,18 @@ void ensure_work(gs_matrix_ &m, size_t bytes, hipStream_t s)
     m.work.alloc(bytes, s);
 }
 
+void *work_for(gs_matrix_ &m, const WorkArea *fixed, size_t bytes, hipStream_t s)
+{
+    if (fixed) {
+        if (bytes > fixed->cap)
+            fail(GS_ERR_UNSUPPORTED, "this SpMM needs %zu bytes of workspace, above the fixed %zu-byte scratch",
+                 bytes, fixed->cap);
+        return fixed->p;
+    }
+    ensure_work(m, bytes, s);
+    return m.work.p;
+}
+
 // Device properties, read once (thread-safe static initialisation; a failed
 // query throws and is retried on the next call).
 int compute_units()

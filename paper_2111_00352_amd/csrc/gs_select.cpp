@@ -34,11 +34,7 @@
 
 namespace gs {
 gs_matrix_ *build_csr(const gs_coo *A, const gs_build_opts &o, hipStream_t s, bool plan);
-void run_spmm(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
-              hipStream_t s);
 void check_coo(const gs_coo *A);
-void check_spmm_args(const gs_matrix_ *A, const float *X, int64_t ldx, const float *Y, int64_t ldy,
-                     int64_t F);
 }  // namespace gs
 
 using namespace gs;

@@ -858,26 +858,29 @@ void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s)
 // --------------------------------------------------------------- launchers
 
 void spmm_csr(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
-              hipStream_t s)
+              hipStream_t s, const WorkArea *fixed)
 {
-    if (!m.csr_planned) plan_csr(m, s);
-    if (spmm_csr_vec4(m, X, ldx, Y, ldy, F, s)) return;
+    if (!m.csr_planned) {
+        if (fixed) fail(GS_ERR_UNSUPPORTED, "CSR handle without a work plan (it is built with the handle)");
+        plan_csr(m, s);
+    }
+    if (spmm_csr_vec4(m, X, ldx, Y, ldy, F, s, fixed)) return;
     const Shape sh = pick_shape(X, ldx, Y, ldy, F);
-    if (m.n_long_chunks) ensure_work(m, (size_t)m.n_long_chunks * F * 4, s);
+    float *work = m.n_long_chunks ? (float *)work_for(m, fixed, (size_t)m.n_long_chunks * F * 4, s) : nullptr;
     dispatch(sh, [&]<int VEC, int G>() {
         constexpr int GPB = kBlock / G;
         if (m.n_items) {
             dim3 grid(u32_grid(ceil_div(m.n_items, GPB)), (unsigned)sh.fslices);
             k_csr_items_generic<VEC, G><<<grid, kBlock, 0, s>>>(
                 m.n_items, m.csr_items.as<int4>(), m.col.as<int32_t>(), m.val.as<float>(), X, ldx, Y,
-                ldy, F, m.work.as<float>());
+                ldy, F, work);
             GS_HIP(hipGetLastError());
         }
         if (m.n_long_rows) {
             dim3 g2(u32_grid(ceil_div(m.n_long_rows, GPB)), (unsigned)sh.fslices);
             k_csr_combine<VEC, G><<<g2, kBlock, 0, s>>>(m.long_rows.as<int32_t>(),
                                                         m.long_first.as<int32_t>(), m.n_long_rows,
-                                                        m.work.as<float>(), Y, ldy, F);
+                                                        work, Y, ldy, F);
             GS_HIP(hipGetLastError());
         }
     });
@@ -959,8 +962,10 @@ int coo_occupancy(CooMainFn fn)
 }  // namespace
 
 void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
-              hipStream_t s)
+              hipStream_t s, const WorkArea *fixed)
 {
+    // the range tables are built (and allocated) per launch shape on first use
+    if (fixed) fail(GS_ERR_UNSUPPORTED, "COO handles are not supported without allocation");
     const Shape sh = pick_shape(X, ldx, Y, ldy, F);
     const CooMain cm = pick_coo_main(sh, m.C, F);  // main pass; the fixup keeps the generic shape
     const int64_t Z = m.Z;
@@ -1047,12 +1052,11 @@ void spmm_coo(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
 }
 
 void spmm_csc(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
-              hipStream_t s)
+              hipStream_t s, const WorkArea *fixed)
 {
     const int64_t n = m.R * F;
     if (n == 0) return;
-    ensure_work(m, (size_t)n * 8, s);
-    double *W = m.work.as<double>();
+    double *W = (double *)work_for(m, fixed, (size_t)n * 8, s);
     auto grid = [](int64_t items) {
         int64_t g = ceil_div(items, (int64_t)kBlock);
         return (unsigned)(g < 1 ? 1 : g > 65536 ? 65536 : g);

@@ -453,7 +453,7 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
 // ------------------------------------------------------------- launcher
 
 bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
-                   hipStream_t s)
+                   hipStream_t s, const WorkArea *fixed)
 {
     auto al = [](const void *p) { return ((uintptr_t)p % 16) == 0; };
     if (F % 4 || ldx % 4 || ldy % 4 || !al(X) || !al(Y)) return false;
@@ -479,7 +479,7 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
         const int64_t n_huge = m.n_long_rows - m.n_medium_rows;
         const int64_t tiles = m.n_medium_rows + ceil_div(n_group_items, GPB);
         if (!tiles) return;
-        if (n_huge) ensure_work(m, (size_t)m.n_long_chunks * F * 4, s);
+        float *work = n_huge ? (float *)work_for(m, fixed, (size_t)m.n_long_chunks * F * 4, s) : nullptr;
         // persistent grid: a few resident workgroups per CU (measured: 4 for
         // length-sorted rows, 8 -- about one tile each -- for natural order)
         const int64_t cap = (int64_t)resident_workgroups() * env_int("GS_WG_MULT", m.csr_sorted ? 4 : 8);
@@ -487,13 +487,13 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
         k_csr_rows<CPL, G, FU><<<grid, kBlock, 0, s>>>(
             m.n_medium_rows, m.long_rows.as<int32_t>(), m.row_ptr.as<int32_t>(), m.csr_chunk,
             n_group_items, m.csr_items.as<int4>() + m.n_medium_chunks, m.col.as<int32_t>(),
-            m.val.as<float>(), X, ldx, Y, ldy, F, m.work.as<float>());
+            m.val.as<float>(), X, ldx, Y, ldy, F, work);
         GS_HIP(hipGetLastError());
         if (n_huge) {
             dim3 g2((unsigned)ceil_div(n_huge, GPB), (unsigned)slices);
             k_csr_combine<CPL, G><<<g2, kBlock, 0, s>>>(m.long_rows.as<int32_t>() + m.n_medium_rows,
                                                         m.long_first.as<int32_t>() + m.n_medium_rows,
-                                                        n_huge, m.work.as<float>(), Y, ldy, F);
+                                                        n_huge, work, Y, ldy, F);
             GS_HIP(hipGetLastError());
         }
     };

@@ -36,6 +36,9 @@ int main(int argc, char **argv)
     expect(gs_build_format(&empty, GS_BSR, &opts, NULL, &m, NULL) == GS_ERR_INVALID_ARG, "BSR block 65");
 
     expect(gs_spmm(NULL, NULL, 1, NULL, 1, 1, NULL) == GS_ERR_INVALID_ARG, "spmm on a null handle");
+    expect(gs_spmm_noalloc(NULL, NULL, 1, NULL, 1, 1, NULL) == GS_ERR_INVALID_ARG,
+           "allocation-free spmm on a null handle");
+    expect(GS_NOALLOC_SCRATCH_BYTES >= (1u << 20), "scratch size is declared");
     gs_matrix_info info;
     expect(gs_get_info(NULL, &info) == GS_ERR_INVALID_ARG, "info on a null handle");
 

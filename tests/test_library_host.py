@@ -45,6 +45,7 @@ def test_null_arguments_rejected_without_gpu(L):
     assert out.value is None
     assert b"gs_coo" in L.gs_last_error()
     assert L.gs_spmm(None, None, 1, None, 1, 1, None) == gs.ERR_INVALID_ARG
+    assert L.gs_spmm_noalloc(None, None, 1, None, 1, 1, None) == gs.ERR_INVALID_ARG
     assert L.gs_to_coo(None, None, None, None, None) == gs.ERR_INVALID_ARG
     assert L.gs_get_info(None, None) == gs.ERR_INVALID_ARG
     coo = gs._Coo(4, 4, 1, None, None, None)  # nnz > 0 with null arrays
