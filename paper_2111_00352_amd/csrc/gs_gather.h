@@ -10,32 +10,57 @@
 
 namespace gs {
 
-// Gathered X rows: plain cached loads (non-temporal loads measured slower:
-// hub rows are reused from L2 and the MALL).
+// Gathered X rows: plain cached loads (non-temporal loads for every row
+// measured slower: hub rows are reused from L2 and the MALL).
 __device__ __forceinline__ float4 load_x4(const float *p)
 {
     return *reinterpret_cast<const float4 *>(p);
 }
 
+// Non-temporal gather of a row that few entries reference: its lines are
+// inserted for early eviction, so they do not push the rows of often
+// referenced columns out of L2.
+__device__ __forceinline__ float4 load_x4_nt(const float *p)
+{
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    const f4 v = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p));
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+
+// Column words with a reference class: bits 27..30 hold the class of the
+// column (bit length of its entry count, at most 15), bits 0..26 the column.
+constexpr int kColClassShift = 27;
+constexpr int kColMask = (1 << kColClassShift) - 1;
+
 // One batch of B entries j .. j+B-1 of the group's current index batch:
 // B X-row loads issued back to back, then B fused multiply-adds.  MASKED
 // batches may run past the last entry m: those slots gather a valid row
 // (lane wrap) and are dropped by a select, so Inf/NaN in X cannot leak in.
-template <int B, int NQ, int G, bool MASKED>
+//
+// CLS: cj holds class-tagged column words; rows of columns whose class is
+// below hot_cls are gathered non-temporally.
+template <int B, int NQ, int G, bool MASKED, bool CLS = false>
 __device__ __forceinline__ void gather_batch(int cj, float vj, int j, int m,
                                              const float *__restrict__ X, int64_t ldx, int64_t c0,
-                                             const bool *qok, float *acc)
+                                             const bool *qok, float *acc, int hot_cls = 0)
 {
     float4 x[B][NQ];
     float v[B];
 #pragma unroll
     for (int u = 0; u < B; u++) {
-        const int cu = __shfl(cj, j + u, G);
+        const int cw = __shfl(cj, j + u, G);
+        const int cu = CLS ? (cw & kColMask) : cw;
         v[u] = __shfl(vj, j + u, G);
         const float *xp = X + (int64_t)cu * ldx + c0;
+        if (CLS && (cw >> kColClassShift) < hot_cls) {
 #pragma unroll
-        for (int q = 0; q < NQ; q++)
-            x[u][q] = qok[q] ? load_x4(xp + 4 * G * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int q = 0; q < NQ; q++)
+                x[u][q] = qok[q] ? load_x4_nt(xp + 4 * G * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+        } else {
+#pragma unroll
+            for (int q = 0; q < NQ; q++)
+                x[u][q] = qok[q] ? load_x4(xp + 4 * G * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
     }
 #pragma unroll
     for (int u = 0; u < B; u++) {

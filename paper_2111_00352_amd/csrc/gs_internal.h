@@ -129,6 +129,11 @@ struct gs_matrix_ {
     int csr_wg_thr = 0;
     bool csr_sorted = false; // items ordered by decreasing length
     bool csr_planned = false; // plan_csr has run (a CSR built only for its features has no plan)
+    // CSR: column indices tagged with their column's reference class (bit
+    // length of its entry count) in bits 27..30, and the number of columns
+    // in each class; empty when the gathers do not use classes
+    gs::DevBuf csr_colf;
+    int64_t col_class_cols[16] = {};
     // COO: rows with no entries (zeroed by the COO fixup launch), and the
     // entries with |col - row| < 4096 (which sets the number of rounds)
     int64_t n_empty_rows = 0;
@@ -234,6 +239,8 @@ void count_blocks_async(const gs_matrix_ &csr, int b, unsigned long long *total,
 // --------------------------------------------------- features (gs_features)
 
 void features_from_csr(const gs_matrix_ &csr, hipStream_t s, gs_features *out);
+// Entry counts cc[0..C) of the columns of col[0..Z) (cc is cleared here).
+void column_counts(const int32_t *col, int64_t C, int64_t Z, int32_t *cc, hipStream_t s);
 // Diagonal occupancy bitmap of a CSR matrix: bit (col - row + R - 1) of
 // bm[ceil((R+C-1)/32)] set for every entry; bm need not be cleared.
 void diag_bitmap(const int32_t *rp, const int32_t *col, int64_t R, int64_t C, int64_t Z,

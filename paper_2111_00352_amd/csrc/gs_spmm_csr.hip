@@ -23,6 +23,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <numeric>
+#include <string>
 #include <vector>
 
 #include "gs_device.h"
@@ -35,12 +36,13 @@ namespace {
 constexpr int kBlock = 256;
 
 // Accumulates the entries [k0, k1) of one row into acc (NQ float4 per lane).
-template <int NQ, int G, int U>
+// CLS: col holds class-tagged column words (see gather_batch).
+template <int NQ, int G, int U, bool CLS>
 __device__ __forceinline__ void gather_entries(const int32_t *__restrict__ col,
                                                const float *__restrict__ val, int64_t k0,
                                                int64_t k1, const float *__restrict__ X,
                                                int64_t ldx, int64_t c0, const bool *qok,
-                                               float *acc, int lane)
+                                               float *acc, int lane, int hot_cls)
 {
     for (int64_t kb = k0; kb < k1; kb += G) {
         const int m = (k1 - kb) < G ? (int)(k1 - kb) : G;
@@ -51,22 +53,23 @@ __device__ __forceinline__ void gather_entries(const int32_t *__restrict__ col,
             vj = ld_stream(val + kb + lane);
         }
         int j = 0;
-        for (; j + U <= m; j += U) gather_batch<U, NQ, G, false>(cj, vj, j, m, X, ldx, c0, qok, acc);
+        for (; j + U <= m; j += U)
+            gather_batch<U, NQ, G, false, CLS>(cj, vj, j, m, X, ldx, c0, qok, acc, hot_cls);
         if (j < m) {
             if (U > 1 && m - j <= U / 2)
-                gather_batch<(U > 1 ? U / 2 : 1), NQ, G, true>(cj, vj, j, m, X, ldx, c0, qok, acc);
+                gather_batch<(U > 1 ? U / 2 : 1), NQ, G, true, CLS>(cj, vj, j, m, X, ldx, c0, qok, acc, hot_cls);
             else
-                gather_batch<U, NQ, G, true>(cj, vj, j, m, X, ldx, c0, qok, acc);
+                gather_batch<U, NQ, G, true, CLS>(cj, vj, j, m, X, ldx, c0, qok, acc, hot_cls);
         }
     }
 }
 
-template <int CPL, int G, bool FULL>
+template <int CPL, int G, bool FULL, bool CLS>
 __global__ __launch_bounds__(kBlock) void k_csr_rows(
     int64_t n_long, const int32_t *__restrict__ long_rows, const int32_t *__restrict__ rp,
     int chunk, int64_t n_short, const int4 *__restrict__ items, const int32_t *__restrict__ col,
     const float *__restrict__ val, const float *__restrict__ X, int64_t ldx, float *__restrict__ Y,
-    int64_t ldy, int64_t F, float *__restrict__ work)
+    int64_t ldy, int64_t F, float *__restrict__ work, int hot_cls)
 {
     constexpr int GPB = kBlock / G;
     constexpr int NQ = CPL / 4;
@@ -92,7 +95,7 @@ __global__ __launch_bounds__(kBlock) void k_csr_rows(
 #pragma unroll
                 for (int i = 0; i < CPL; i++) part_acc[i] = 0.0f;
                 const int64_t ce = cs + chunk < e ? cs + chunk : e;
-                gather_entries<NQ, G, U>(col, val, cs, ce, X, ldx, c0, qok, part_acc, lane);
+                gather_entries<NQ, G, U, CLS>(col, val, cs, ce, X, ldx, c0, qok, part_acc, lane, hot_cls);
 #pragma unroll
                 for (int i = 0; i < CPL; i++) acc[i] += part_acc[i];
             }
@@ -123,7 +126,8 @@ __global__ __launch_bounds__(kBlock) void k_csr_rows(
             const int64_t it = (t - n_long) * GPB + g;
             if (it >= n_short) break;  // later tiles of this workgroup are past the end too
             const int4 d = items[it];
-            gather_entries<NQ, G, U>(col, val, d.y, (int64_t)d.y + d.z, X, ldx, c0, qok, acc, lane);
+            gather_entries<NQ, G, U, CLS>(col, val, d.y, (int64_t)d.y + d.z, X, ldx, c0, qok, acc, lane,
+                                          hot_cls);
             if (d.w < 0)
                 store_row_stream<NQ, G>(Y + (int64_t)d.x * ldy + c0, qok, acc);
             else  // a chunk of a huge row: its partial sum, added later in slot order
@@ -351,7 +355,64 @@ __global__ void k_pick3(const int32_t *__restrict__ cnt, int64_t a, int64_t b, i
     }
 }
 
+// Reference class of a column with n entries: the bit length of n, at most 15.
+__device__ __forceinline__ int col_class(int n)
+{
+    const int b = 32 - __clz(n);
+    return b < 15 ? b : 15;
+}
+
+// Columns per reference class (16 bins, added into hist).
+__global__ __launch_bounds__(kBlock) void k_class_hist(const int32_t *__restrict__ cc, int64_t C,
+                                                       int32_t *__restrict__ hist)
+{
+    __shared__ int h[16];
+    if (threadIdx.x < 16) h[threadIdx.x] = 0;
+    __syncthreads();
+    for (int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x; j < C; j += (int64_t)gridDim.x * kBlock)
+        atomicAdd(&h[col_class(cc[j])], 1);
+    __syncthreads();
+    if (threadIdx.x < 16 && h[threadIdx.x]) atomicAdd(&hist[threadIdx.x], h[threadIdx.x]);
+}
+
+// Class-tagged copy of the column indices: col | class(count of col) << 27.
+__global__ __launch_bounds__(kBlock) void k_tag_cols(const int32_t *__restrict__ col, int64_t Z,
+                                                     const int32_t *__restrict__ cc, int32_t *__restrict__ tagged)
+{
+    for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < Z; e += (int64_t)gridDim.x * kBlock) {
+        const int c = col[e];
+        tagged[e] = c | (col_class(cc[c]) << kColClassShift);
+    }
+}
+
 }  // namespace
+
+// Reference classes of the columns, for gathers that keep often referenced X
+// rows in L2: counts per column, the number of columns in each class (read
+// back) and the class-tagged column copy.  Built for skewed matrices (rows
+// ordered by length; GS_CSR_HOTCOLD = on / off forces it) whose column count
+// fits the 27-bit column field.
+void plan_col_classes(gs_matrix_ &m, hipStream_t s)
+{
+    const char *e = std::getenv("GS_CSR_HOTCOLD");
+    const bool on = e && *e ? std::string(e) == "on" : m.csr_sorted;
+    if (!on || m.Z == 0 || m.C > kColMask + 1) return;
+    DevBuf cc, hist;
+    cc.alloc((size_t)m.C * 4, s);
+    hist.alloc(16 * 4, s);
+    column_counts(m.col.as<int32_t>(), m.C, m.Z, cc.as<int32_t>(), s);
+    GS_HIP(hipMemsetAsync(hist.p, 0, 16 * 4, s));
+    k_class_hist<<<plan_grid(m.C), kBlock, 0, s>>>(cc.as<int32_t>(), m.C, hist.as<int32_t>());
+    GS_HIP(hipGetLastError());
+    m.csr_colf.alloc((size_t)m.Z * 4, s);
+    k_tag_cols<<<plan_grid(m.Z), kBlock, 0, s>>>(m.col.as<int32_t>(), m.Z, cc.as<int32_t>(),
+                                                 m.csr_colf.as<int32_t>());
+    GS_HIP(hipGetLastError());
+    int32_t h[16];
+    GS_HIP(hipMemcpyAsync(h, hist.p, sizeof h, hipMemcpyDeviceToHost, s));
+    GS_HIP(hipStreamSynchronize(s));
+    for (int c = 0; c < 16; c++) m.col_class_cols[c] = h[c];
+}
 
 void plan_csr(gs_matrix_ &m, hipStream_t s)
 {
@@ -447,6 +508,7 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
     } else {
         GS_HIP(hipMemsetAsync(m.long_first.p, 0, 4, s));
     }
+    plan_col_classes(m, s);
     m.csr_planned = true;
 }
 
@@ -471,6 +533,23 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
     const int g = lanes <= 4 ? 4 : lanes <= 8 ? 8 : lanes <= 16 ? 16 : lanes <= 32 ? 32 : 64;
     const int64_t slices = ceil_div(F, (int64_t)g * cpl);
     const bool full = (F % ((int64_t)g * cpl)) == 0;
+    // Reference classes: the rows of the most referenced columns, whole
+    // classes of them up to GS_CSR_HOT_KB (64 MiB) at this width, are
+    // gathered with plain loads, every other row non-temporally, so that
+    // rows read a few times do not displace them from the memory-side cache.
+    // Measured on the 2M-row power-law graph at F = 128 (52M entries, rows
+    // of columns with at least 64 entries hot): 3426 -> 3126 us; budgets of
+    // 4 / 32 / 128 / 256 MiB gave 4185 / 3286 / 3231 / 3306 us.  Not used
+    // when the rows of every referenced column fit the budget.
+    int hot_cls = 0;
+    if (m.csr_colf.p && cpl == 4) {
+        const int64_t budget = (int64_t)env_int("GS_CSR_HOT_KB", 65536) * 1024 / (F * 4);
+        int64_t cum = 0;
+        for (int c = 15; c >= 1 && !hot_cls; c--) {
+            cum += m.col_class_cols[c];
+            if (cum > budget) hot_cls = c < 15 ? c + 1 : 15;
+        }
+    }
     auto launch = [&](auto cpl_t, auto g_t, auto full_t) {
         constexpr int CPL = decltype(cpl_t)::value, G = decltype(g_t)::value;
         constexpr bool FU = decltype(full_t)::value;
@@ -484,11 +563,22 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
         // length-sorted rows, 8 -- about one tile each -- for natural order)
         const int64_t cap = (int64_t)resident_workgroups() * env_int("GS_WG_MULT", m.csr_sorted ? 4 : 8);
         dim3 grid((unsigned)std::max<int64_t>(1, std::min(tiles, cap / slices)), (unsigned)slices);
-        k_csr_rows<CPL, G, FU><<<grid, kBlock, 0, s>>>(
-            m.n_medium_rows, m.long_rows.as<int32_t>(), m.row_ptr.as<int32_t>(), m.csr_chunk,
-            n_group_items, m.csr_items.as<int4>() + m.n_medium_chunks, m.col.as<int32_t>(),
-            m.val.as<float>(), X, ldx, Y, ldy, F, work);
-        GS_HIP(hipGetLastError());
+        if constexpr (CPL == 4) {
+            if (hot_cls) {
+                k_csr_rows<CPL, G, FU, true><<<grid, kBlock, 0, s>>>(
+                    m.n_medium_rows, m.long_rows.as<int32_t>(), m.row_ptr.as<int32_t>(), m.csr_chunk,
+                    n_group_items, m.csr_items.as<int4>() + m.n_medium_chunks, m.csr_colf.as<int32_t>(),
+                    m.val.as<float>(), X, ldx, Y, ldy, F, work, hot_cls);
+                GS_HIP(hipGetLastError());
+            }
+        }
+        if (!(CPL == 4 && hot_cls)) {
+            k_csr_rows<CPL, G, FU, false><<<grid, kBlock, 0, s>>>(
+                m.n_medium_rows, m.long_rows.as<int32_t>(), m.row_ptr.as<int32_t>(), m.csr_chunk,
+                n_group_items, m.csr_items.as<int4>() + m.n_medium_chunks, m.col.as<int32_t>(),
+                m.val.as<float>(), X, ldx, Y, ldy, F, work, 0);
+            GS_HIP(hipGetLastError());
+        }
         if (n_huge) {
             dim3 g2((unsigned)ceil_div(n_huge, GPB), (unsigned)slices);
             k_csr_combine<CPL, G><<<g2, kBlock, 0, s>>>(m.long_rows.as<int32_t>() + m.n_medium_rows,

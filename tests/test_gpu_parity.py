@@ -575,6 +575,33 @@ def test_csr_plan_thresholds(monkeypatch, thr, chunk, wg, sort):
     check_spmm(case, m, graphgen.features_x(C, 20, 26, "normal"))
 
 
+@pytest.mark.parametrize("hot_kb", ["1", "16", "64"])
+@pytest.mark.parametrize("sort", ["1", "2"])
+def test_csr_reference_classes(monkeypatch, hot_kb, sort):
+    # gathers chosen by the column's reference class: a small hot budget puts
+    # most X rows on the non-temporal path.  The class tags live in a copy of
+    # the column indices, so the handle's arrays stay canonical, and the load
+    # kind changes no result: Y equals the untagged path's bit for bit.
+    monkeypatch.setenv("GS_CSR_SORT", sort)
+    monkeypatch.setenv("GS_CSR_HOTCOLD", "off")
+    g = graphgen.scaled(2)
+    case = _case_from_graph(g)
+    plain = case.build("csr")
+    monkeypatch.setenv("GS_CSR_HOTCOLD", "on")
+    monkeypatch.setenv("GS_CSR_HOT_KB", hot_kb)
+    m = check_layout(case, "csr")
+    for F in (64, 128, 132):
+        X = graphgen.features_x(case.C, F, 70 + F, "normal")
+        check_spmm(case, m, X)
+        Xd = _dev(X)
+        assert (_bits(_host(m.spmm(Xd))) == _bits(_host(plain.spmm(Xd)))).all()
+    # hub rows of every tier with the classes on
+    R, C = 700, 5000
+    row, col, val = graphgen.dense_rows_coo(R, C, [0, 3, 350, 699], seed=27, base_nnz=8000)
+    case = Case(R, C, row, col, val)
+    check_spmm(case, case.build("csr"), graphgen.features_x(C, 64, 28, "normal"))
+
+
 @pytest.mark.parametrize("F", [16, 48, 80, 512, 1040])
 def test_bsr16_matrix_core_widths(monkeypatch, F):
     # 16x16 blocks run on the matrix cores for F a multiple of 16 (wide F
