@@ -240,6 +240,48 @@ def other_workload(gs, k, dev, stream, reps):
             "selector": selector_summary(fmts, chosen), "formats": fmts}
 
 
+def gather_ceiling(gs, dev, stream, reps=10):
+    """Random-gather ceiling of the CSR kernel: one million rows of 16
+    entries each whose columns are spread uniformly over an X of S bytes
+    (F = 128), for S from 2 MiB (fits one XCD's L2) through 256 MiB (the
+    memory-side cache) to 1 GiB.  Entries of row i are (h_i + k s_i) mod C,
+    k < 16, with h_i uniform and s_i odd (no duplicates for C a power of two).
+    Reports the median SpMM time, the requested gather rate Z F 4 / t and the
+    B_alg roofline fraction.  Plain gathers (no reference classes)."""
+    import torch
+
+    os.environ["GS_CSR_HOTCOLD"] = "off"
+    R, d, F = 1 << 20, 16, 128
+    gen = torch.Generator(device="cpu").manual_seed(15)
+    rows = []
+    for mib in (2, 4, 16, 64, 128, 256, 512, 1024):
+        C = mib * 2**20 // (F * 4)
+        h = torch.randint(0, C, (R, 1), generator=gen, dtype=torch.int64)
+        st = torch.randint(0, C // 2, (R, 1), generator=gen, dtype=torch.int64) * 2 + 1
+        colm = (h + torch.arange(d, dtype=torch.int64)[None, :] * st) % C
+        row = torch.arange(R, dtype=torch.int32).repeat_interleave(d).to(dev)
+        col = colm.reshape(-1).to(torch.int32).to(dev)
+        val = torch.ones(R * d, dtype=torch.float32, device=dev)
+        m = gs.build_format(row, col, val, (R, C), "csr")
+        X = torch.randn((C, F), generator=gen).to(dev)
+        Ys = [torch.empty((R, F), device=dev) for _ in range(2)]
+        pairs = [(X, y) for y in Ys]
+        for i in range(3):
+            m.spmm(X, out=Ys[i % 2])
+        (dd,) = event_durations([lambda p: m.spmm(p[0], out=p[1])], stream, reps, pairs)
+        t = float(np.median(dd))
+        Z = R * d
+        rows.append({"x_mib": mib, "n_cols": C, "median_us": round(t * 1e6, 1),
+                     "gather_gbs": round(Z * F * 4 / t / 1e9, 1),
+                     "roofline_frac": round(b_alg(R, C, Z, F) / t / 1e9 / HBM_PEAK_GBS, 4)})
+        log(f"gather ceiling X {mib} MiB: {rows[-1]}")
+        m.close()
+        del m, X, Ys, pairs, row, col, val
+        torch.cuda.empty_cache()
+    os.environ.pop("GS_CSR_HOTCOLD", None)
+    return {"rows": R, "entries_per_row": d, "F": F, "table": rows}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -255,6 +297,8 @@ def main():
     ap.add_argument("--format-reps", type=int, default=20)
     ap.add_argument("--no-gcn", action="store_true", help="skip the two-layer GCN end-to-end run")
     ap.add_argument("--gcn-epochs", type=int, default=10)
+    ap.add_argument("--gather-ceiling", action="store_true",
+                    help="only the random-gather ceiling table of the CSR kernel (X of 2 MiB .. 1 GiB)")
     ap.add_argument("--profile-run", action="store_true",
                     help="only the warm-up and timed steps plus a 256 MiB calibration copy (for rocprofv3)")
     args = ap.parse_args()
@@ -274,6 +318,9 @@ def main():
     torch.backends.cuda.matmul.allow_tf32 = False
     dev = torch.device("cuda", 0)
     stream = torch.cuda.current_stream()
+    if args.gather_ceiling:
+        print(json.dumps({"gather_ceiling": gather_ceiling(gs, dev, stream)}), flush=True)
+        return
     k = args.config
     two_layer = k == 5
 
