@@ -134,6 +134,11 @@ struct gs_matrix_ {
     // in each class; empty when the gathers do not use classes
     gs::DevBuf csr_colf;
     int64_t col_class_cols[16] = {};
+    // CSR: entries inside their row tile's window, per candidate tile of 32,
+    // 64, 128 and 256 rows with halo 0 / 1 (natural-order matrices without
+    // long rows only; win_counted says whether they were counted)
+    bool win_counted = false;
+    int64_t win_entries[8] = {};
     // COO: rows with no entries (zeroed by the COO fixup launch), and the
     // entries with |col - row| < 4096 (which sets the number of rounds)
     int64_t n_empty_rows = 0;

@@ -35,6 +35,10 @@ namespace {
 
 constexpr int kBlock = 256;
 
+// Candidate row tiles of the LDS-staged kernel: 32 << k rows, k < kWinCands,
+// each with halo 0 and 1.
+constexpr int kWinCands = 4;
+
 // Accumulates the entries [k0, k1) of one row into acc (NQ float4 per lane).
 // CLS: col holds class-tagged column words (see gather_batch).
 template <int NQ, int G, int U, bool CLS>
@@ -190,6 +194,98 @@ __global__ __launch_bounds__(kBlock) void k_csr_combine(const int32_t *__restric
         }
     }
     store_row_stream<NQ, G>(Y + (int64_t)rows[r] * ldy + c0, qok, acc);
+}
+
+// Row tiles with their X window staged in LDS (natural row order, rows of at
+// most the short-row limit).  A workgroup takes T consecutive rows [r0, r1)
+// and first copies the X rows [r0 - halo, r1 + halo) of its column slice
+// into LDS with coalesced loads; its groups then run the rows as the plain
+// kernel does, reading every entry whose column lies in the window from LDS
+// and the others from global memory.  Graphs whose edges stay mostly inside
+// such tiles (communities of consecutive nodes, stencils) then gather most
+// X rows once per tile instead of once per entry through L2.
+template <int CPL, int G, bool FULL>
+__global__ __launch_bounds__(kBlock) void k_csr_window(
+    int64_t R, int64_t C, const int32_t *__restrict__ rp, const int32_t *__restrict__ col,
+    const float *__restrict__ val, const float *__restrict__ X, int64_t ldx, float *__restrict__ Y,
+    int64_t ldy, int64_t F, int T, int halo, int64_t ntiles)
+{
+    constexpr int GPB = kBlock / G;
+    constexpr int NQ = CPL / 4;
+    constexpr int RW = G * NQ;  // float4 per staged row
+    constexpr int B0 = 32 / CPL > 0 ? 32 / CPL : 1;
+    constexpr int B = B0 < G ? B0 : G;  // X rows in flight per batch
+    extern __shared__ float4 xs[];
+    const int g = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t cbase = (int64_t)blockIdx.y * (G * CPL);
+    const int64_t c0 = cbase + (int64_t)lane * 4;
+    bool qok[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; q++) qok[q] = FULL || (c0 + 4 * G * q < F);
+
+    for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const int64_t r0 = t * T, r1 = r0 + T < R ? r0 + T : R;
+        const int64_t w0 = r0 - halo > 0 ? r0 - halo : 0;
+        const int64_t w1 = r1 + halo < C ? r1 + halo : C;
+        const int W = w1 > w0 ? (int)(w1 - w0) : 0;
+        __syncthreads();  // the previous tile's rows are done with xs
+        for (int idx = threadIdx.x; idx < W * RW; idx += kBlock) {
+            const int wr = idx / RW, j = idx - wr * RW;
+            const int64_t cc = cbase + 4 * j;
+            xs[idx] = (FULL || cc < F) ? load_x4(X + (w0 + wr) * ldx + cc) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        __syncthreads();
+        for (int64_t r = r0 + g; r < r1; r += GPB) {
+            float acc[CPL];
+#pragma unroll
+            for (int i = 0; i < CPL; i++) acc[i] = 0.0f;
+            const int64_t s = rp[r], e = rp[r + 1];
+            for (int64_t kb = s; kb < e; kb += G) {
+                const int m = (e - kb) < G ? (int)(e - kb) : G;
+                int cj = 0;
+                float vj = 0.0f;
+                if (lane < m) {
+                    cj = ld_stream(col + kb + lane);
+                    vj = ld_stream(val + kb + lane);
+                }
+                for (int j = 0; j < m; j += B) {
+                    float4 x[B][NQ];
+                    float v[B];
+#pragma unroll
+                    for (int u = 0; u < B; u++) {
+                        const int cu = __shfl(cj, j + u, G);
+                        v[u] = __shfl(vj, j + u, G);
+                        if (cu >= w0 && cu < w1) {
+                            const float4 *xr = xs + (int64_t)(cu - w0) * RW + lane;
+#pragma unroll
+                            for (int q = 0; q < NQ; q++) x[u][q] = xr[q * G];
+                        } else {
+                            const float *xp = X + (int64_t)cu * ldx + c0;
+#pragma unroll
+                            for (int q = 0; q < NQ; q++)
+                                x[u][q] = qok[q] ? load_x4(xp + 4 * G * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+                        }
+                    }
+#pragma unroll
+                    for (int u = 0; u < B; u++) {
+                        const bool live = j + u < m;
+#pragma unroll
+                        for (int q = 0; q < NQ; q++) {
+                            const float a0 = __builtin_fmaf(v[u], x[u][q].x, acc[4 * q + 0]);
+                            const float a1 = __builtin_fmaf(v[u], x[u][q].y, acc[4 * q + 1]);
+                            const float a2 = __builtin_fmaf(v[u], x[u][q].z, acc[4 * q + 2]);
+                            const float a3 = __builtin_fmaf(v[u], x[u][q].w, acc[4 * q + 3]);
+                            acc[4 * q + 0] = live ? a0 : acc[4 * q + 0];
+                            acc[4 * q + 1] = live ? a1 : acc[4 * q + 1];
+                            acc[4 * q + 2] = live ? a2 : acc[4 * q + 2];
+                            acc[4 * q + 3] = live ? a3 : acc[4 * q + 3];
+                        }
+                    }
+                }
+            }
+            store_row_stream<NQ, G>(Y + r * ldy + c0, qok, acc);
+        }
+    }
 }
 
 int env_int(const char *name, int dflt)
@@ -385,7 +481,56 @@ __global__ __launch_bounds__(kBlock) void k_tag_cols(const int32_t *__restrict__
     }
 }
 
+// Entries whose column lies in their row's tile window, for the row tiles
+// of 32 << k rows with halo 0 (counts[2k]) and halo 1 (counts[2k+1]):
+// one partial set per workgroup, added into counts.
+__global__ __launch_bounds__(kBlock) void k_win_counts(const int32_t *__restrict__ rp,
+                                                       const int32_t *__restrict__ col, int64_t R, int64_t C,
+                                                       unsigned long long *__restrict__ counts)
+{
+    __shared__ unsigned long long t64[kBlock / kWave];
+    unsigned long long n[2 * kWinCands] = {};
+    for (int64_t r = (int64_t)blockIdx.x * kBlock + threadIdx.x; r < R; r += (int64_t)gridDim.x * kBlock) {
+        for (int64_t k = rp[r]; k < rp[r + 1]; k++) {
+            const int64_t c = col[k];
+#pragma unroll
+            for (int w = 0; w < kWinCands; w++) {
+                const int64_t T = 32 << w;
+                const int64_t b = r / T * T, top = b + T < R ? b + T : R;
+                n[2 * w] += (c >= b && c < top) ? 1u : 0u;
+                n[2 * w + 1] += (c >= b - 1 && c < top + 1) ? 1u : 0u;
+            }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 2 * kWinCands; i++) {
+        const unsigned long long tot = block_sum_u64<kBlock>(n[i], t64);
+        if (threadIdx.x == 0 && tot) atomicAdd(&counts[i], tot);
+    }
+}
+
 }  // namespace
+
+// Locality of the row tiles: how many entries fall in their tile's window
+// for each candidate tile and halo (read back), for the LDS-staged kernel.
+// Counted for natural-order matrices without long rows (GS_CSR_WINDOW = off
+// skips it).
+void plan_windows(gs_matrix_ &m, hipStream_t s)
+{
+    const char *e = std::getenv("GS_CSR_WINDOW");
+    if ((e && std::string(e) == "off") || m.csr_sorted || m.n_long_rows > 0 || m.Z == 0) return;
+    DevBuf cnt;
+    cnt.alloc(sizeof(unsigned long long) * 2 * kWinCands, s);
+    GS_HIP(hipMemsetAsync(cnt.p, 0, cnt.bytes, s));
+    k_win_counts<<<stats_grid(m.R), kBlock, 0, s>>>(m.row_ptr.as<int32_t>(), m.col.as<int32_t>(), m.R, m.C,
+                                                    cnt.as<unsigned long long>());
+    GS_HIP(hipGetLastError());
+    unsigned long long h[2 * kWinCands];
+    GS_HIP(hipMemcpyAsync(h, cnt.p, sizeof h, hipMemcpyDeviceToHost, s));
+    GS_HIP(hipStreamSynchronize(s));
+    for (int i = 0; i < 2 * kWinCands; i++) m.win_entries[i] = (int64_t)h[i];
+    m.win_counted = true;
+}
 
 // Reference classes of the columns, for gathers that keep often referenced X
 // rows in L2: counts per column, the number of columns in each class (read
@@ -509,6 +654,7 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
         GS_HIP(hipMemsetAsync(m.long_first.p, 0, 4, s));
     }
     plan_col_classes(m, s);
+    plan_windows(m, s);
     m.csr_planned = true;
 }
 
@@ -550,10 +696,51 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
             if (cum > budget) hot_cls = c < 15 ? c + 1 : 15;
         }
     }
+    // LDS-staged row tiles: the candidate (tile, halo) that keeps the most
+    // entries in the window within GS_CSR_WIN_KB (32 KiB) of LDS per
+    // workgroup, when at least half the entries are in it.  More LDS per
+    // workgroup costs resident waves: on the block-community graph (F = 256)
+    // tiles of 32 / 64 / 128 rows (32 / 64 / 128 KiB) measured 193 / 280 /
+    // 480 us against 209 us without staging.
+    int win_T = 0, win_h = 0;
+    if (m.win_counted && m.n_long_rows == 0) {
+        const int64_t lds_cap = std::min<int64_t>(max_lds_bytes(), (int64_t)env_int("GS_CSR_WIN_KB", 32) * 1024);
+        const int64_t min_in = m.Z * env_int("GS_CSR_WIN_PCT", 50) / 100;
+        int64_t best = -1;
+        for (int w = 0; w < kWinCands; w++)
+            for (int h = 0; h < 2; h++) {
+                const int64_t bytes = (int64_t)((32 << w) + 2 * h) * g * cpl * 4;
+                const int64_t in = m.win_entries[2 * w + h];
+                if (bytes <= lds_cap && in >= min_in && in > best) {
+                    best = in;
+                    win_T = 32 << w;
+                    win_h = h;
+                }
+            }
+        if (const char *e = std::getenv("GS_CSR_WIN_T"); e && *e) {  // tests and sweeps: force a tile
+            const char *hh = std::getenv("GS_CSR_WIN_H");
+            const int t = std::atoi(e), h = hh && std::atoi(hh) > 0 ? 1 : 0;
+            if (t > 0 && (int64_t)(t + 2 * h) * g * cpl * 4 <= max_lds_bytes()) {
+                win_T = t;
+                win_h = h;
+            }
+        }
+    }
     auto launch = [&](auto cpl_t, auto g_t, auto full_t) {
         constexpr int CPL = decltype(cpl_t)::value, G = decltype(g_t)::value;
         constexpr bool FU = decltype(full_t)::value;
         constexpr int GPB = kBlock / G;
+        if (win_T > 0) {
+            const int64_t ntiles = ceil_div(m.R, win_T);
+            const size_t lds = (size_t)(win_T + 2 * win_h) * G * CPL * 4;
+            const int64_t cap = (int64_t)resident_workgroups() * env_int("GS_WG_MULT", 8);
+            dim3 grid((unsigned)std::max<int64_t>(1, std::min(ntiles, cap / slices)), (unsigned)slices);
+            k_csr_window<CPL, G, FU><<<grid, kBlock, lds, s>>>(m.R, m.C, m.row_ptr.as<int32_t>(),
+                                                               m.col.as<int32_t>(), m.val.as<float>(), X, ldx, Y,
+                                                               ldy, F, win_T, win_h, ntiles);
+            GS_HIP(hipGetLastError());
+            return;
+        }
         const int64_t n_group_items = m.n_items - m.n_medium_chunks;  // huge chunks + short rows
         const int64_t n_huge = m.n_long_rows - m.n_medium_rows;
         const int64_t tiles = m.n_medium_rows + ceil_div(n_group_items, GPB);

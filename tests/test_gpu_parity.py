@@ -602,6 +602,29 @@ def test_csr_reference_classes(monkeypatch, hot_kb, sort):
     check_spmm(case, case.build("csr"), graphgen.features_x(C, 64, 28, "normal"))
 
 
+@pytest.mark.parametrize("T,h", [("32", "0"), ("64", "1"), ("256", "1"), ("96", "0")])
+def test_csr_lds_window_tiles(monkeypatch, T, h):
+    # row tiles with their X window staged in LDS: communities of consecutive
+    # nodes and a stencil (entries inside and outside the window), tiles cut
+    # across communities (96 rows), ragged last tile, several column slices,
+    # strided operands, rectangular matrices whose windows run past the last
+    # column or are empty
+    monkeypatch.setenv("GS_CSR_WIN_T", T)
+    monkeypatch.setenv("GS_CSR_WIN_H", h)
+    for k in (4, 3):
+        g = graphgen.scaled(k)
+        case = _case_from_graph(g)
+        m = case.build("csr")
+        check_spmm(case, m, g.X)
+        check_spmm(case, m, graphgen.features_x(case.C, 36, 80 + k, "normal"), ldx_pad=4, ldy_pad=8)
+        check_spmm(case, m, graphgen.features_x(case.C, 520, 90 + k, "normal"))
+    for R, C, seed in ((1003, 517, 81), (517, 1003, 82), (2000, 2000, 83)):
+        case = _random_case(R, C, 9000, seed, empty=0.2)
+        m = case.build("csr")
+        check_spmm(case, m, graphgen.features_x(C, 64, seed + 5, "normal"))
+        check_spmm(case, m, graphgen.features_x(C, 132, seed + 6, "normal"))
+
+
 @pytest.mark.parametrize("F", [16, 48, 80, 512, 1040])
 def test_bsr16_matrix_core_widths(monkeypatch, F):
     # 16x16 blocks run on the matrix cores for F a multiple of 16 (wide F
