@@ -200,6 +200,13 @@ int gs_get_array(gs_matrix A, int which, const void **dev_ptr, uint64_t *bytes);
  * of dst_bytes >= the array's size.  Asynchronous on s. */
 int gs_copy_array(gs_matrix A, int which, void *dst, uint64_t dst_bytes, gs_stream s);
 
+/* Frees A's device arrays and workspace through the hooks that allocated
+ * them, in the order of the stream A was built on.  When A was last read on
+ * another stream (gs_spmm, gs_spmm_noalloc, gs_to_coo, gs_copy_array), the
+ * call first waits for that work to finish, so no later allocation on the
+ * build stream can reuse the memory under it.  Work captured into a graph
+ * is not tracked: destroy A only after the graph's last replay.  NULL is
+ * ignored. */
 void gs_destroy(gs_matrix A);
 
 /* Matrix features of Table 2 (Sec. 4.4), extracted on the device from the

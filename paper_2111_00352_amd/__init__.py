@@ -22,7 +22,7 @@ import torch
 
 __all__ = [
     "FORMATS", "FORMAT_NAMES", "GnnSpmmError", "Matrix", "SelectContext", "build_format",
-    "extract_features", "lib", "library_path", "FEATURE_NAMES",
+    "extract_features", "lib", "library_path", "FEATURE_NAMES", "set_allocator",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -92,6 +92,10 @@ ERR_INFEASIBLE, ERR_OOM, ERR_HIP, ERR_MODEL, ERR_UNSUPPORTED = -5, -6, -7, -8, -
 
 _lib = None
 _alloc_keep = None
+# Every hook set ever installed through set_allocator, kept for the life of
+# the process: the library frees each buffer through the hooks that
+# allocated it, so a collected callback would be called after it is gone.
+_hooks_alive: list = []
 
 
 def library_path() -> str:
@@ -150,10 +154,12 @@ def _require_gpu():
     _install_torch_allocator()
 
 
-def _install_torch_allocator():
+def _install_torch_allocator(reinstall: bool = False):
     """Routes the library's device allocations through PyTorch's caching allocator."""
     global _alloc_keep
     if _alloc_keep is not None:
+        if reinstall:
+            _check(lib().gs_set_allocator(ctypes.byref(_alloc_keep[0])))
         return
 
     def _alloc(nbytes, stream, _ctx):
@@ -168,6 +174,38 @@ def _install_torch_allocator():
     a = _Allocator(_ALLOC_FN(_alloc), _FREE_FN(_free), None)
     _check(lib().gs_set_allocator(ctypes.byref(a)))
     _alloc_keep = (a, _alloc, _free)
+
+
+def set_allocator(alloc=None, free=None):
+    """Installs device allocation hooks for all later library allocations
+    (gs_set_allocator).  alloc(nbytes, stream) returns a device pointer
+    (int) aligned to 256 bytes, or 0 / None when it cannot allocate;
+    free(ptr, stream) releases one; both must be stream-ordered (see
+    gs_allocator).  No arguments reinstall PyTorch's caching allocator.
+
+    Buffers always go back through the hooks that allocated them, so the
+    hooks must outlive every handle built with them: this binding keeps each
+    hook set (the callables and their ctypes wrappers) referenced until the
+    process ends, whatever the caller does with its own references."""
+    if (alloc is None) != (free is None):
+        raise ValueError("alloc and free must both be given or both be None")
+    if alloc is None:
+        _install_torch_allocator(reinstall=True)
+        return
+
+    def _a(nbytes, stream, _ctx):
+        try:
+            p = alloc(int(nbytes), int(stream or 0))
+        except Exception:  # reported by the library as GS_ERR_OOM
+            return None
+        return int(p) if p else None
+
+    def _f(ptr, stream, _ctx):
+        free(int(ptr), int(stream or 0))
+
+    hooks = _Allocator(_ALLOC_FN(_a), _FREE_FN(_f), None)
+    _hooks_alive.append((hooks, _a, _f, alloc, free))
+    _check(lib().gs_set_allocator(ctypes.byref(hooks)))
 
 
 def _stream(stream=None) -> int:

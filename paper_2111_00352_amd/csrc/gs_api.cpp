@@ -76,6 +76,7 @@ void run_spmm(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
     case GS_CSC: spmm_csc(m, X, ldx, Y, ldy, F, s, fixed); break;
     default: fail(GS_ERR_INVALID_ARG, "corrupt matrix handle");
     }
+    note_use(m, s);
 }
 
 }  // namespace gs
@@ -147,6 +148,7 @@ int gs_to_coo(gs_matrix A, int32_t *row, int32_t *col, float *val, gs_stream str
         if (!A) fail(GS_ERR_INVALID_ARG, "null matrix handle");
         if (A->Z > 0 && (!row || !col || !val)) fail(GS_ERR_INVALID_ARG, "null output array");
         to_coo(*A, row, col, val, (hipStream_t)stream);
+        note_use(*A, (hipStream_t)stream);
     });
 }
 

@@ -157,6 +157,23 @@ struct gs_matrix_ {
     gs::DevBuf work;
 
     uint64_t device_bytes = 0;
+
+    // Work that reads the handle's arrays on a stream other than `stream`
+    // (an SpMM, to_coo or an array copy): an event recorded after the last
+    // such call, waited for before the arrays are freed (they are freed in
+    // `stream` order, which does not cover other streams).
+    hipEvent_t last_foreign = nullptr;
+
+    gs_matrix_() = default;
+    gs_matrix_(const gs_matrix_ &) = delete;
+    gs_matrix_ &operator=(const gs_matrix_ &) = delete;
+    ~gs_matrix_()
+    {
+        if (last_foreign) {
+            (void)hipEventSynchronize(last_foreign);
+            (void)hipEventDestroy(last_foreign);
+        }
+    }
 };
 
 namespace gs {
@@ -307,6 +324,11 @@ struct WorkArea {
 // given (GS_ERR_UNSUPPORTED when bytes exceed fixed->cap), else m.work grown
 // in stream order.
 void *work_for(gs_matrix_ &m, const WorkArea *fixed, size_t bytes, hipStream_t s);
+
+// Records that work reading m's arrays was enqueued on s (see
+// gs_matrix_::last_foreign); nothing when s is m's own stream or is being
+// captured into a graph (replays are ordered by the caller).
+void note_use(gs_matrix_ &m, hipStream_t s);
 
 // Argument checks of gs_spmm (throws Error) and the format dispatch.
 void check_spmm_args(const gs_matrix_ *A, const float *X, int64_t ldx, const float *Y, int64_t ldy,

@@ -89,6 +89,19 @@ void *work_for(gs_matrix_ &m, const WorkArea *fixed, size_t bytes, hipStream_t s
     return m.work.p;
 }
 
+void note_use(gs_matrix_ &m, hipStream_t s)
+{
+    if (s == m.stream) return;
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cs) != hipSuccess) {  // e.g. the legacy stream during a capture
+        (void)hipGetLastError();
+        return;
+    }
+    if (cs != hipStreamCaptureStatusNone) return;
+    if (!m.last_foreign) GS_HIP(hipEventCreateWithFlags(&m.last_foreign, hipEventDisableTiming));
+    GS_HIP(hipEventRecord(m.last_foreign, s));
+}
+
 // Device properties, read once (thread-safe static initialisation; a failed
 // query throws and is retried on the next call).
 int compute_units()
@@ -200,8 +213,10 @@ int gs_copy_array(gs_matrix A, int which, void *dst, uint64_t dst_bytes, gs_stre
         return GS_ERR_INVALID_ARG;
     }
     return guarded([&] {
-        if (bytes)
+        if (bytes) {
             GS_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, (hipStream_t)s));
+            note_use(*A, (hipStream_t)s);
+        }
     });
 }
 

@@ -522,6 +522,30 @@ def test_work_stays_on_the_callers_stream():
     assert all(feats[k] == v for k, v in ints.items()) and feats["f"] == f.tolist()
 
 
+def test_destroy_right_after_spmm_on_another_stream():
+    # a handle built on the default stream, multiplied on a second stream and
+    # destroyed at once: the destroy waits for that SpMM before its arrays go
+    # back to the allocator, so the default stream's next allocations (which
+    # may take the same memory) cannot overwrite them under the running SpMM
+    gs._require_gpu()
+    case = _random_case(20000, 20000, 600000, 91, empty=0.0)
+    X = graphgen.features_x(case.C, 128, 92, "normal")
+    Xd = _dev(X)
+    Yref, M = oracle.spmm(case.R, case.rp, case.ccol, case.cval, X)
+    s2 = torch.cuda.Stream()
+    for fmt in ("csc", "coo", "csr"):
+        m = case.build(fmt)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s2):
+            Y = m.spmm(Xd)
+        m.close()
+        junk = [torch.full((1 << 20,), float("nan"), device=DEV) for _ in range(16)]
+        s2.synchronize()
+        ok, worst = oracle.check_spmm(_host(Y), Yref, M)
+        assert ok, f"{fmt}: worst |err|/bound {worst}"
+        del junk
+
+
 # -------------------------------------------------------------- conversion
 
 @pytest.mark.parametrize("src", FMTS)

@@ -208,3 +208,29 @@ def test_footprints_match_the_library_sizes():
     X, T, _, _ = train.load(DATA_PATH)
     R, Z = X[:, 0], X[:, 2]
     assert np.allclose(M[:, 0], 4 * (R + 1) + 8 * Z) and np.allclose(M[:, 1], 12 * Z)
+
+
+def test_set_allocator_keeps_hooks_alive(L):
+    # the binding keeps every installed hook set referenced: the caller may
+    # drop its own callables at once, and a handle built with them can still
+    # free its buffers through them later (no GPU needed: nothing allocates)
+    import gc
+    import weakref
+
+    class Hook:
+        def __call__(self, *args):
+            return None
+
+    a, f = Hook(), Hook()
+    wa, wf = weakref.ref(a), weakref.ref(f)
+    gs.set_allocator(a, f)
+    del a, f
+    gc.collect()
+    assert wa() is not None and wf() is not None
+    assert any(h[3] is wa() for h in gs._hooks_alive)
+    with pytest.raises(ValueError):
+        gs.set_allocator(lambda n, s: 0)
+    gs.set_allocator()  # back to PyTorch's caching allocator
+    assert gs._alloc_keep is not None
+    gc.collect()
+    assert wa() is not None  # still kept after the switch

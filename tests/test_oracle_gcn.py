@@ -103,3 +103,39 @@ def test_relu_ambiguity_bound_covers_a_flipped_decision():
     extra, count = gcn.relu_ambiguity(g, X, ref, mag, eps=r[i, h] * 1.0001)
     assert count >= 1
     assert np.all(np.abs(dW1_flipped - ref["dW1"]) <= extra * (1 + 1e-9) + 1e-15)
+
+
+def _atol_branch_holds(relu_ambiguity):
+    """The absolute term of the ambiguity test (atol, the 1e-6 absolute part
+    of the SpMM bound) on its own: with eps = 0 the ReLU input of smallest
+    magnitude is ambiguous exactly when atol reaches |P1[i, h]|, and the
+    bound then covers flipping that decision."""
+    g, _, X, W1, W2, T = _problem(n=30, nnz=120, seed=14)
+    ref = gcn.forward_backward(g, X, W1, W2, T)
+    mag = gcn.magnitudes(g, X, W1, W2, T)
+    a = np.abs(ref["P1"])
+    a[mag["P1"] == 0] = np.inf  # exact zeros of empty rows are never ambiguous in the check
+    i, h = np.unravel_index(np.argmin(a), a.shape)
+    p = a[i, h]
+    mask = ref["P1"] > 0
+    mask[i, h] = not mask[i, h]
+    dW1_flipped = X.T @ g.agg_t(ref["dH1"] * mask)
+    extra, count = relu_ambiguity(g, X, ref, mag, eps=0.0, atol=p * 1.0001)
+    _, count_below = relu_ambiguity(g, X, ref, mag, eps=0.0, atol=p * 0.9999)
+    covered = np.all(np.abs(dW1_flipped - ref["dW1"]) <= extra * (1 + 1e-9) + 1e-15)
+    return count >= 1 and count_below == count - 1 and bool(covered)
+
+
+def test_relu_ambiguity_absolute_term():
+    assert _atol_branch_holds(gcn.relu_ambiguity)
+
+
+def test_relu_ambiguity_planted_sign_mistake_is_caught():
+    # the absolute term subtracted instead of added: the entry within atol of
+    # zero is no longer ambiguous, and the bound misses its flip
+    def planted(g, X, ref, mag, eps, atol=0.0):
+        amb = np.abs(ref["P1"]) <= eps * mag["P1"] - atol
+        E = np.abs(mag["dH1"]) * amb
+        return np.abs(np.asarray(X, dtype=np.float64)).T @ g.agg_t(E, absolute=True), int(amb.sum())
+
+    assert not _atol_branch_holds(planted)
