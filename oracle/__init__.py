@@ -42,12 +42,21 @@ INT_NAMES = [
 ]
 
 
+# ORACLE_SANITIZE=1: a separate build with AddressSanitizer and
+# UndefinedBehaviorSanitizer (the process must preload the ASan runtime).
+_SANITIZE = os.environ.get("ORACLE_SANITIZE") == "1"
+if _SANITIZE:
+    _LIB = os.path.join(_HERE, "liboracle_san.so")
+_SAN_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined", "-fno-sanitize-recover=all"]
+
+
 def build(force: bool = False) -> str:
     """Compile oracle.c into liboracle.so with gcc (OpenMP for the SpMM loop)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
+        opt = _SAN_FLAGS if _SANITIZE else ["-O2"]
         subprocess.check_call(
-            ["gcc", "-O2", "-fopenmp", "-std=c11", "-Wall", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"]
+            ["gcc", *opt, "-fopenmp", "-std=c11", "-Wall", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"]
         )
         os.replace(tmp, _LIB)
     return _LIB
