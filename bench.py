@@ -299,6 +299,8 @@ def main():
     ap.add_argument("--gcn-epochs", type=int, default=10)
     ap.add_argument("--gather-ceiling", action="store_true",
                     help="only the random-gather ceiling table of the CSR kernel (X of 2 MiB .. 1 GiB)")
+    ap.add_argument("--format", default=None,
+                    help="time this format (fixed selector) instead of the predicted one, for profiling")
     ap.add_argument("--profile-run", action="store_true",
                     help="only the warm-up and timed steps plus a 256 MiB calibration copy (for rocprofv3)")
     args = ap.parse_args()
@@ -337,7 +339,7 @@ def main():
     library_init_s = library_warmup(gs, dev, F)
 
     # ---- selector, layer 1: first call (features + prediction + conversion)
-    ctx = gs.SelectContext("model")
+    ctx = gs.SelectContext("fixed", fixed=args.format) if args.format else gs.SelectContext("model")
     Y0 = torch.empty((R, F), dtype=torch.float32, device=dev)
     t0 = time.perf_counter()
     _, chosen1 = ctx.run(1, row, col, val, (R, C), X0, out=Y0)

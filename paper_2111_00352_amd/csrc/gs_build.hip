@@ -1076,6 +1076,7 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
                 GS_HIP(hipMemcpyAsync(&dense, dn.p, sizeof dense, hipMemcpyDeviceToHost, s));
                 GS_HIP(hipStreamSynchronize(s));
                 m->n_dense_blocks = (int64_t)dense;
+                plan_bsr_hybrid(*m, rp, col, val, s);
             }
             m->device_bytes = need;
             break;

@@ -115,6 +115,12 @@ struct gs_matrix_ {
     int64_t nb = 0;
     gs::DevBuf bptr, bcol, bval, bmask;  // bmask: per block 64-bit mask of nonzero columns
     int64_t n_dense_blocks = 0;
+    // BSR(16) hybrid plan: the dense blocks of each block row (indices into
+    // the block arrays; hyb_dptr[nbr+1]) and the entries of every other block
+    // as a CSR of their own (hyb_rrp[R+1], hyb_rcol, hyb_rval)
+    bool hyb_planned = false;
+    int64_t hyb_ndense = 0, hyb_nrest = 0;
+    gs::DevBuf hyb_dptr, hyb_didx, hyb_rrp, hyb_rcol, hyb_rval;
 
     // Kernel plans built once per matrix.
     // CSR: rows longer than the short-row limit, split into chunks.
@@ -197,6 +203,9 @@ constexpr int kCooSnap = 32;
 constexpr int kCooFold = 128;
 constexpr int kCooMinRange = 32;
 constexpr int kCooBandRange = 48;
+// BSR(16) hybrid plan: a block with at least this many entries (of 256)
+// runs on the matrix cores, the entries of sparser blocks as a row list.
+constexpr int kHybridDenseMin = 64;
 // A 16x16 BSR block with at least this many stored columns counts as dense.
 constexpr int kBsrDenseCols = 8;
 
@@ -303,6 +312,10 @@ bool spmm_ell_fast(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
                    hipStream_t s);
 bool spmm_dia_fast(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
                    hipStream_t s);
+
+// Hybrid plan of a 16x16 BSR handle from its CSR arrays (dense blocks on the
+// matrix cores, the rest as rows); GS_BSR_HYBRID = off skips it.
+void plan_bsr_hybrid(gs_matrix_ &m, const int32_t *rp, const int32_t *col, const float *val, hipStream_t s);
 
 // 16x16-block BSR on the matrix cores; false when b != 16 or F % 16 != 0.
 bool spmm_bsr16_mfma(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,

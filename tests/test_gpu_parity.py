@@ -649,6 +649,26 @@ def test_csr_lds_window_tiles(monkeypatch, T, h):
         check_spmm(case, m, graphgen.features_x(C, 132, seed + 6, "normal"))
 
 
+@pytest.mark.parametrize("dense_min", ["1", "64", "256", "300"])
+@pytest.mark.parametrize("ht", ["", "1", "8"])
+def test_bsr16_hybrid_plan(monkeypatch, dense_min, ht):
+    # dense 16x16 blocks on the matrix cores, every other block's entries as a
+    # row list: block communities (dense and sparse blocks), a stencil, random
+    # matrices with R, C not multiples of 16 and empty rows; every block dense
+    # (1), the default cut (64), only full blocks (256) and none (300); tiles
+    # per wave forced to 1 and 8; widths over one and several column groups.
+    # The block arrays stay canonical.
+    monkeypatch.setenv("GS_BSR_DENSE_MIN", dense_min)
+    if ht:
+        monkeypatch.setenv("GS_BSR_HT", ht)
+    cases = [_case_from_graph(graphgen.scaled(4)), _case_from_graph(graphgen.scaled(3)),
+             _random_case(1001, 997, 12000, 63, empty=0.1)]
+    for i, case in enumerate(cases):
+        m = check_layout(case, "bsr", 16)
+        for F in (16, 48, 272):
+            check_spmm(case, m, graphgen.features_x(case.C, F, 64 + F + i, "normal"), ldx_pad=4 * (i == 2))
+
+
 @pytest.mark.parametrize("F", [16, 48, 80, 512, 1040])
 def test_bsr16_matrix_core_widths(monkeypatch, F):
     # 16x16 blocks run on the matrix cores for F a multiple of 16 (wide F
