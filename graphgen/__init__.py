@@ -380,6 +380,30 @@ def training_matrix(i: int):
     return n, row, col, np.ones(row.size, np.float32), dict(kind="random01", density=d)
 
 
+EVAL_SIZE_RANGE = (1000, 60000)
+
+
+def evaluation_matrix(i: int):
+    """Evaluation matrix i (0..99) of the held-out set with random float
+    values: square, n log-uniform in 1,000..60,000 (beyond the training
+    sizes, up to the size of the paper's largest dataset), density
+    log-uniform in 0.01%..10% (nnz capped at 30M), stored values random
+    floats in (0, 1] (the (0,1) recipe rounded to fp32).  Never used for
+    training."""
+    rng = _rng(70_000 + i)
+    lo, hi = EVAL_SIZE_RANGE
+    n = int(round(float(np.exp(rng.uniform(np.log(lo), np.log(hi))))))
+    d = float(np.exp(rng.uniform(np.log(1e-4), np.log(0.1))))
+    d = min(d, TRAIN_NNZ_CAP / float(n * n))
+    if d > 0.02:
+        row, col = _bernoulli_rows(rng, n, d)
+    else:
+        k = max(1, int(rng.binomial(n * n, d)))
+        keys = np.unique(rng.integers(0, n * n, size=k, dtype=np.int64))
+        row, col = (keys // n).astype(np.int32), (keys % n).astype(np.int32)
+    return n, row, col, _u01_open(rng, row.size), dict(kind="random-float", density=d)
+
+
 def structured_matrix(i: int):
     """Structured training matrix i: banded, community-block, power-law and
     grid patterns, values 1.  Matrices 0..119 have 10^4..2x10^5 rows,

@@ -9,6 +9,10 @@
 namespace gs {
 
 constexpr int kWave = 64;  // CDNA wavefront width
+// Every sequential fp32 sum runs at most this many terms before it is added
+// into a running total (a row's rounding error then stays within 1e-5 of
+// the sum of its absolute terms for rows of thousands of entries).
+constexpr int kChainFold = 128;
 constexpr int kXcds = 8;   // MI355X: 8 accelerator dies, each with its own L2
 
 // The dispatcher hands consecutive workgroup ids to the XCDs round-robin.

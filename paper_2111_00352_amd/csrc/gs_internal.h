@@ -194,6 +194,9 @@ constexpr int kCsrChunk = 128;
 // Long rows up to this many entries take one workgroup on the vectorised
 // path; longer ones are split across workgroups.
 constexpr int kCsrWgRow = 1024;
+// With many more long rows than resident workgroups, rows up to this many
+// entries take one lane group each (summed in chunks of kCsrChunk).
+constexpr int kCsrGroupRow = 2048;
 // COO: range boundaries move to the next row start within at most kCooSnap
 // entries, and a segment's running sum is folded every kCooFold entries;
 // ranges hold at least kCooMinRange entries, and about kCooBandRange when

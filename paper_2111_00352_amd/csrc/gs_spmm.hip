@@ -128,7 +128,12 @@ __global__ __launch_bounds__(kBlock) void k_csr_items_generic(
     const int64_t it = (int64_t)blockIdx.x * GPB + g;
     if (it >= n_items) return;
     const int4 d = items[it];
-    Acc<VEC> acc = gather_range<VEC, G>(col, val, d.y, (int64_t)d.y + d.z, X, ldx, c0, active, lane);
+    // rows of the group tier are summed kChainFold entries at a time
+    Acc<VEC> acc;
+    acc.zero();
+    for (int64_t cs = d.y, e = (int64_t)d.y + d.z; cs < e; cs += kChainFold)
+        acc.add(gather_range<VEC, G>(col, val, cs, cs + kChainFold < e ? cs + kChainFold : e, X, ldx, c0, active,
+                                     lane));
     if (!active) return;
     if (d.w < 0)
         st_vec_stream<VEC>(Y + (int64_t)d.x * ldy + c0, acc.vec());
@@ -603,10 +608,17 @@ __global__ __launch_bounds__(kBlock) void k_ell(int64_t R, int64_t K, const int3
     const int64_t row = xcd_tile(blockIdx.x, n_tiles) * GPB + g;
     if (row >= R) return;
     const int gbase = (threadIdx.x % kWave) / G * G;
-    Acc<VEC> a0, a1;
+    Acc<VEC> a0, a1, tot;
     a0.zero();
     a1.zero();
+    tot.zero();
     for (int64_t kb = 0; kb < K; kb += G) {
+        if (kb > 0 && kb % kChainFold == 0) {  // fold the running chains every kChainFold slots
+            tot.add(a0);
+            tot.add(a1);
+            a0.zero();
+            a1.zero();
+        }
         const int64_t k = kb + lane;
         int cj = -1;
         float vj = 0.0f;
@@ -636,8 +648,9 @@ __global__ __launch_bounds__(kBlock) void k_ell(int64_t R, int64_t K, const int3
         }
         if (n < G) break;
     }
-    a0.add(a1);
-    if (active) st_vec_stream<VEC>(Y + row * ldy + c0, a0.vec());
+    tot.add(a0);
+    tot.add(a1);
+    if (active) st_vec_stream<VEC>(Y + row * ldy + c0, tot.vec());
 }
 
 // ---------------------------------------------------------------- DIA
@@ -658,11 +671,18 @@ __global__ __launch_bounds__(kBlock) void k_dia(int64_t R, int64_t C, int64_t ND
     const bool active = c0 < F;
     const int64_t row = xcd_tile(blockIdx.x, n_tiles) * GPB + g;
     if (row >= R) return;
-    Acc<VEC> a0, a1;
+    Acc<VEC> a0, a1, tot;
     a0.zero();
     a1.zero();
+    tot.zero();
     int64_t d = 0;
     for (; d + 2 <= ND; d += 2) {
+        if (d > 0 && d % kChainFold == 0) {  // fold the running chains every kChainFold diagonals
+            tot.add(a0);
+            tot.add(a1);
+            a0.zero();
+            a1.zero();
+        }
         const int64_t j0 = row + offsets[d], j1 = row + offsets[d + 1];
         const float v0 = ld_stream(data + d * R + row);
         const float v1 = ld_stream(data + (d + 1) * R + row);
@@ -676,8 +696,9 @@ __global__ __launch_bounds__(kBlock) void k_dia(int64_t R, int64_t C, int64_t ND
         const float v0 = ld_stream(data + d * R + row);
         if (active && v0 != 0.0f && j0 >= 0 && j0 < C) a0.fma(v0, ld_vec<VEC>(X + j0 * ldx + c0));
     }
-    a0.add(a1);
-    if (active) st_vec_stream<VEC>(Y + row * ldy + c0, a0.vec());
+    tot.add(a0);
+    tot.add(a1);
+    if (active) st_vec_stream<VEC>(Y + row * ldy + c0, tot.vec());
 }
 
 // ---------------------------------------------------------------- BSR
@@ -703,10 +724,21 @@ __global__ __launch_bounds__(kBlock) void k_bsr(int64_t R, int64_t C, int b, int
     const bool active = c0 < F;
     const int64_t br = xcd_tile(blockIdx.x, nbr);
     const int bb = b * b;
-    Acc<VEC> acc[RPT];
+    Acc<VEC> acc[RPT], tot[RPT];
 #pragma unroll
-    for (int r = 0; r < RPT; r++) acc[r].zero();
+    for (int r = 0; r < RPT; r++) {
+        acc[r].zero();
+        tot[r].zero();
+    }
+    const int64_t fold = kChainFold / b > 0 ? kChainFold / b : 1;  // blocks per running chain
     for (int64_t blk = bptr[br]; blk < bptr[br + 1]; blk++) {
+        if (blk > bptr[br] && (blk - bptr[br]) % fold == 0) {
+#pragma unroll
+            for (int r = 0; r < RPT; r++) {
+                tot[r].add(acc[r]);
+                acc[r].zero();
+            }
+        }
         __syncthreads();
         for (int t = threadIdx.x; t < bb; t += kBlock) blk_lds[t] = ld_stream(bval + blk * bb + t);
         __syncthreads();
@@ -727,9 +759,10 @@ __global__ __launch_bounds__(kBlock) void k_bsr(int64_t R, int64_t C, int b, int
     if (!active) return;
 #pragma unroll
     for (int r = 0; r < RPT; r++) {
+        tot[r].add(acc[r]);
         const int rr = g + r * RG;
         const int64_t row = br * b + rr;
-        if (rr < b && row < R) st_vec_stream<VEC>(Y + row * ldy + c0, acc[r].vec());
+        if (rr < b && row < R) st_vec_stream<VEC>(Y + row * ldy + c0, tot[r].vec());
     }
 }
 

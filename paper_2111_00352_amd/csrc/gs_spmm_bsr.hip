@@ -39,6 +39,8 @@ constexpr int kBlock = 256;
 // path; sparser ones are cheaper on the vector ALUs (an fp32 16x16x4 MFMA
 // costs as much as 16 wave-wide FMAs per 4 block columns).
 constexpr int kDenseCols = kBsrDenseCols;
+// Blocks per running chain of an accumulator (16 products each).
+constexpr int kFoldBlocks = kChainFold / 16;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 template <int T, int NB, bool WROWS>
@@ -67,13 +69,20 @@ __global__ __launch_bounds__(kBlock) void k_bsr16_mfma(int64_t R, int64_t nbr,
     for (int64_t u = xcd_tile(blockIdx.x, gridDim.x); u < units; u += gridDim.x) {
         const int64_t br = WROWS ? u * 4 + wave : u;
         if (br >= nbr) break;
-        f32x4 acc[T];
+        f32x4 acc[T], tot[T];
 #pragma unroll
-        for (int t = 0; t < T; t++) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int t = 0; t < T; t++) acc[t] = tot[t] = f32x4{0.f, 0.f, 0.f, 0.f};
         const int64_t b0 = bptr[br], b1 = bptr[br + 1];
         // NB blocks per iteration: every load of the batch (masks, block
         // values, X rows) is issued before the first MFMA consumes one.
         for (int64_t blk = b0; blk < b1; blk += NB) {
+            if (blk > b0 && (blk - b0) % kFoldBlocks == 0) {  // 16 terms per block into the running chain
+#pragma unroll
+                for (int t = 0; t < T; t++) {
+                    tot[t] += acc[t];
+                    acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+                }
+            }
             uint64_t mask[NB];
             int64_t xr0[NB];
             float av[NB][4];
@@ -144,11 +153,12 @@ __global__ __launch_bounds__(kBlock) void k_bsr16_mfma(int64_t R, int64_t nbr,
         }
 #pragma unroll
         for (int t = 0; t < T; t++) {
+            tot[t] += acc[t];
             if (!tok[t]) continue;
 #pragma unroll
             for (int i = 0; i < 4; i++) {
                 const int64_t row = br * 16 + 4 * kk + i;
-                if (row < R) __builtin_nontemporal_store(acc[t][i], Y + row * ldy + xcol + 16 * t);
+                if (row < R) __builtin_nontemporal_store(tot[t][i], Y + row * ldy + xcol + 16 * t);
             }
         }
     }
@@ -195,11 +205,18 @@ __global__ __launch_bounds__(kBlock) void k_bsr16_hybrid(
     for (int64_t u = xcd_tile(blockIdx.x, gridDim.x); u < units; u += gridDim.x) {
         const int64_t br = u * 4 + wave;
         if (br >= nbr) break;
-        f32x4 acc[T];
+        f32x4 acc[T], tot[T];
 #pragma unroll
-        for (int t = 0; t < T; t++) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int t = 0; t < T; t++) acc[t] = tot[t] = f32x4{0.f, 0.f, 0.f, 0.f};
         const int64_t d0 = dptr[br], d1 = dptr[br + 1];
         for (int64_t d = d0; d < d1; d += NB) {
+            if (d > d0 && (d - d0) % kFoldBlocks == 0) {  // 16 terms per block into the running chain
+#pragma unroll
+                for (int t = 0; t < T; t++) {
+                    tot[t] += acc[t];
+                    acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+                }
+            }
             uint64_t mask[NB];
             int64_t xr0[NB];
             float av[NB][4];
@@ -240,9 +257,11 @@ __global__ __launch_bounds__(kBlock) void k_bsr16_hybrid(
         // accumulator layout (lane m + 16 kk: rows 4kk..4kk+3, column m of
         // each tile) -> row-major tile in this wave's LDS rows
 #pragma unroll
-        for (int t = 0; t < T; t++)
+        for (int t = 0; t < T; t++) {
+            tot[t] += acc[t];
 #pragma unroll
-            for (int i = 0; i < 4; i++) tl[(4 * kk + i) * LDT + 16 * t + m] = acc[t][i];
+            for (int i = 0; i < 4; i++) tl[(4 * kk + i) * LDT + 16 * t + m] = tot[t][i];
+        }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -252,7 +271,15 @@ __global__ __launch_bounds__(kBlock) void k_bsr16_hybrid(
             float4 a = *reinterpret_cast<const float4 *>(tl + i * LDT + 4 * gl);
             if (row < R) {
                 const int64_t k0 = rrp[row], k1 = rrp[row + 1];
+                float4 run = make_float4(0.f, 0.f, 0.f, 0.f);  // the current chain of at most kChainFold terms
                 for (int64_t kb = k0; kb < k1; kb += G) {
+                    if (kb > k0 && (kb - k0) % kChainFold == 0) {
+                        a.x += run.x;
+                        a.y += run.y;
+                        a.z += run.z;
+                        a.w += run.w;
+                        run = make_float4(0.f, 0.f, 0.f, 0.f);
+                    }
                     const int mm = (k1 - kb) < G ? (int)(k1 - kb) : G;
                     int cj = 0;
                     float vj = 0.0f;
@@ -273,17 +300,21 @@ __global__ __launch_bounds__(kBlock) void k_bsr16_hybrid(
 #pragma unroll
                         for (int e = 0; e < U; e++) {
                             const bool live = j + e < mm;
-                            const float a0 = __builtin_fmaf(v[e], x[e].x, a.x);
-                            const float a1 = __builtin_fmaf(v[e], x[e].y, a.y);
-                            const float a2 = __builtin_fmaf(v[e], x[e].z, a.z);
-                            const float a3 = __builtin_fmaf(v[e], x[e].w, a.w);
-                            a.x = live ? a0 : a.x;
-                            a.y = live ? a1 : a.y;
-                            a.z = live ? a2 : a.z;
-                            a.w = live ? a3 : a.w;
+                            const float a0 = __builtin_fmaf(v[e], x[e].x, run.x);
+                            const float a1 = __builtin_fmaf(v[e], x[e].y, run.y);
+                            const float a2 = __builtin_fmaf(v[e], x[e].z, run.z);
+                            const float a3 = __builtin_fmaf(v[e], x[e].w, run.w);
+                            run.x = live ? a0 : run.x;
+                            run.y = live ? a1 : run.y;
+                            run.z = live ? a2 : run.z;
+                            run.w = live ? a3 : run.w;
                         }
                     }
                 }
+                a.x += run.x;
+                a.y += run.y;
+                a.z += run.z;
+                a.w += run.w;
                 if (cok) {
                     float *yp = Y + row * ldy + c2;
                     __builtin_nontemporal_store(a.x, yp);

@@ -130,8 +130,21 @@ __global__ __launch_bounds__(kBlock) void k_csr_rows(
             const int64_t it = (t - n_long) * GPB + g;
             if (it >= n_short) break;  // later tiles of this workgroup are past the end too
             const int4 d = items[it];
-            gather_entries<NQ, G, U, CLS>(col, val, d.y, (int64_t)d.y + d.z, X, ldx, c0, qok, acc, lane,
-                                          hot_cls);
+            if (d.z <= chunk) {
+                gather_entries<NQ, G, U, CLS>(col, val, d.y, (int64_t)d.y + d.z, X, ldx, c0, qok, acc, lane,
+                                              hot_cls);
+            } else {  // a row of up to the group limit: chunk by chunk, each summed in fresh registers
+                const int64_t e = (int64_t)d.y + d.z;
+                for (int64_t cs = d.y; cs < e; cs += chunk) {
+                    float part_acc[CPL];
+#pragma unroll
+                    for (int i = 0; i < CPL; i++) part_acc[i] = 0.0f;
+                    gather_entries<NQ, G, U, CLS>(col, val, cs, cs + chunk < e ? cs + chunk : e, X, ldx, c0, qok,
+                                                  part_acc, lane, hot_cls);
+#pragma unroll
+                    for (int i = 0; i < CPL; i++) acc[i] += part_acc[i];
+                }
+            }
             if (d.w < 0)
                 store_row_stream<NQ, G>(Y + (int64_t)d.x * ldy + c0, qok, acc);
             else  // a chunk of a huge row: its partial sum, added later in slot order
@@ -236,11 +249,18 @@ __global__ __launch_bounds__(kBlock) void k_csr_window(
         }
         __syncthreads();
         for (int64_t r = r0 + g; r < r1; r += GPB) {
-            float acc[CPL];
+            float acc[CPL], tot[CPL];
 #pragma unroll
-            for (int i = 0; i < CPL; i++) acc[i] = 0.0f;
+            for (int i = 0; i < CPL; i++) acc[i] = tot[i] = 0.0f;
             const int64_t s = rp[r], e = rp[r + 1];
             for (int64_t kb = s; kb < e; kb += G) {
+                if (kb > s && (kb - s) % kChainFold == 0) {  // fold the running chain
+#pragma unroll
+                    for (int i = 0; i < CPL; i++) {
+                        tot[i] += acc[i];
+                        acc[i] = 0.0f;
+                    }
+                }
                 const int m = (e - kb) < G ? (int)(e - kb) : G;
                 int cj = 0;
                 float vj = 0.0f;
@@ -283,7 +303,9 @@ __global__ __launch_bounds__(kBlock) void k_csr_window(
                     }
                 }
             }
-            store_row_stream<NQ, G>(Y + r * ldy + c0, qok, acc);
+#pragma unroll
+            for (int i = 0; i < CPL; i++) tot[i] += acc[i];
+            store_row_stream<NQ, G>(Y + r * ldy + c0, qok, tot);
         }
     }
 }
@@ -319,13 +341,13 @@ namespace {
 
 struct PlanStats {
     unsigned long long sum, sum2;
-    int maxlen, n_long, n_huge;
+    int maxlen, n_long, n_huge, n_group;
 };
 
 // Row-length statistics: one partial record per workgroup (a one-workgroup
 // grid writes the result itself); k_plan_stats_final combines the partials.
 __device__ __forceinline__ PlanStats block_plan_stats(unsigned long long sum, unsigned long long sum2, int mx,
-                                                      int nl, int nh)
+                                                      int nl, int nh, int ng)
 {
     __shared__ unsigned long long t64[kBlock / kWave];
     __shared__ int t32[kBlock / kWave];
@@ -335,16 +357,17 @@ __device__ __forceinline__ PlanStats block_plan_stats(unsigned long long sum, un
     p.maxlen = block_max_i32<kBlock>(mx, t32);
     p.n_long = (int)block_sum_u64<kBlock>((unsigned long long)nl, t64);
     p.n_huge = (int)block_sum_u64<kBlock>((unsigned long long)nh, t64);
+    p.n_group = (int)block_sum_u64<kBlock>((unsigned long long)ng, t64);
     return p;
 }
 
 __global__ __launch_bounds__(kBlock) void k_plan_stats(const int32_t *__restrict__ rp, int64_t R,
-                                                       int thr, int wg_thr,
+                                                       int thr, int wg_thr, int group_max,
                                                        PlanStats *__restrict__ part,
                                                        PlanStats *__restrict__ st)
 {
     unsigned long long sum = 0, sum2 = 0;
-    int mx = 0, nl = 0, nh = 0;
+    int mx = 0, nl = 0, nh = 0, ng = 0;
     for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < R;
          i += (int64_t)gridDim.x * kBlock) {
         const int len = rp[i + 1] - rp[i];
@@ -353,8 +376,9 @@ __global__ __launch_bounds__(kBlock) void k_plan_stats(const int32_t *__restrict
         mx = len > mx ? len : mx;
         nl += len > thr;
         nh += len > wg_thr;
+        ng += len > group_max;
     }
-    const PlanStats p = block_plan_stats(sum, sum2, mx, nl, nh);
+    const PlanStats p = block_plan_stats(sum, sum2, mx, nl, nh, ng);
     if (threadIdx.x == 0) (gridDim.x == 1 ? *st : part[blockIdx.x]) = p;
 }
 
@@ -362,7 +386,7 @@ __global__ __launch_bounds__(kBlock) void k_plan_stats_final(const PlanStats *__
                                                              PlanStats *__restrict__ st)
 {
     unsigned long long sum = 0, sum2 = 0;
-    int mx = 0, nl = 0, nh = 0;
+    int mx = 0, nl = 0, nh = 0, ng = 0;
     for (int64_t g = threadIdx.x; g < G; g += kBlock) {
         const PlanStats q = part[g];
         sum += q.sum;
@@ -370,8 +394,9 @@ __global__ __launch_bounds__(kBlock) void k_plan_stats_final(const PlanStats *__
         mx = q.maxlen > mx ? q.maxlen : mx;
         nl += q.n_long;
         nh += q.n_huge;
+        ng += q.n_group;
     }
-    const PlanStats p = block_plan_stats(sum, sum2, mx, nl, nh);
+    const PlanStats p = block_plan_stats(sum, sum2, mx, nl, nh, ng);
     if (threadIdx.x == 0) *st = p;
 }
 
@@ -569,13 +594,15 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
     const int64_t R = m.R;
     const int32_t *rp = m.row_ptr.as<int32_t>();
 
-    PlanStats st = {0, 0, 0, 0, 0};
+    const int group_max = std::max(env_int("GS_CSR_GROUP_ROW", kCsrGroupRow), thr);
+    PlanStats st = {0, 0, 0, 0, 0, 0};
     if (R > 0) {
         const unsigned G = stats_grid(R);
         DevBuf d_st, part;
         d_st.alloc(sizeof st, s);
         if (G > 1) part.alloc(sizeof(PlanStats) * G, s);
-        k_plan_stats<<<G, kBlock, 0, s>>>(rp, R, thr, wg_thr, part.as<PlanStats>(), d_st.as<PlanStats>());
+        k_plan_stats<<<G, kBlock, 0, s>>>(rp, R, thr, wg_thr, group_max, part.as<PlanStats>(),
+                                          d_st.as<PlanStats>());
         GS_HIP(hipGetLastError());
         if (G > 1) {
             k_plan_stats_final<<<1, kBlock, 0, s>>>(part.as<PlanStats>(), G, d_st.as<PlanStats>());
@@ -594,16 +621,26 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
     m.csr_sorted = sorted;
     // A workgroup per medium row pays off for a few hub rows running beside
     // the short ones; with more medium rows than resident workgroups they
-    // would queue behind each other with most of each workgroup idle, so then
-    // every long row is cut into chunk items instead.
-    int wg_thr_eff = wg_thr;
-    int64_t n_huge = st.n_huge;
-    if (st.n_long - st.n_huge > resident_workgroups()) {
+    // would queue behind each other with most of each workgroup idle, so
+    // then every long row is cut into chunk items whose partial sums a second
+    // launch adds.  With many more (at least 8 per resident workgroup), every
+    // row of up to group_max entries instead takes one lane group, which sums
+    // it chunk by chunk in registers: the rows alone fill the groups, and no
+    // partial sum goes through memory.  Measured on uniform random matrices
+    // of 18-50k rows of 300-1500 entries at F = 128: 1.3-1.6x faster than
+    // chunk items; with 9-13k such rows chunk items stay ahead at F = 64.
+    int thr_eff = thr, wg_thr_eff = wg_thr;
+    int64_t n_long = st.n_long, n_huge = st.n_huge;
+    const int64_t n_medium = st.n_long - st.n_huge;
+    const int64_t group_min = env_int("GS_CSR_GROUP_MIN", resident_workgroups() * 8);
+    if (n_medium > group_min && group_max > thr) {
+        thr_eff = wg_thr_eff = group_max;
+        n_long = n_huge = st.n_group;
+    } else if (n_medium > resident_workgroups()) {
         wg_thr_eff = thr;
         n_huge = st.n_long;
     }
     m.csr_wg_thr = wg_thr_eff;
-    const int64_t n_long = st.n_long;
     m.n_long_rows = n_long;
     m.n_medium_rows = n_long - n_huge;
     m.n_short = R - n_long;
@@ -613,15 +650,15 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
     uint32_t *perm = nullptr;
     if (R > 0) {
         // ranks are at most max(longest row, thr): L bits, the group above them
-        const int L = bits_for(std::max(st.maxlen, thr));
+        const int L = bits_for(std::max(st.maxlen, thr_eff));
         uint64_t *keys = nullptr;
         if (sorted || n_long > 0) {  // otherwise every key is equal: natural order, no sort
             ka.alloc((size_t)R * 8, s);
             kb.alloc((size_t)R * 8, s);
             pa.alloc((size_t)R * 4, s);
             pb.alloc((size_t)R * 4, s);
-            k_plan_keys<<<plan_grid(R), kBlock, 0, s>>>(rp, R, thr, wg_thr_eff, sorted ? 1 : 0, st.maxlen, L,
-                                                        ka.as<uint64_t>());
+            k_plan_keys<<<plan_grid(R), kBlock, 0, s>>>(rp, R, thr_eff, wg_thr_eff, sorted ? 1 : 0, st.maxlen,
+                                                        L, ka.as<uint64_t>());
             GS_HIP(hipGetLastError());
             std::vector<int> shifts;
             for (int sft = 0; sft < L + 2; sft += 8) shifts.push_back(sft);

@@ -47,10 +47,17 @@ __global__ __launch_bounds__(kBlock) void k_ell_fast(int64_t R, int64_t K,
     for (int64_t tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
         const int64_t row = tile * GPB + g;
         if (row >= R) break;
-        float acc[CPL];
+        float acc[CPL], tot[CPL];
 #pragma unroll
-        for (int i = 0; i < CPL; i++) acc[i] = 0.0f;
+        for (int i = 0; i < CPL; i++) acc[i] = tot[i] = 0.0f;
         for (int64_t kb = 0; kb < K; kb += G) {
+            if (kb > 0 && kb % kChainFold == 0) {  // fold the running chain every kChainFold slots
+#pragma unroll
+                for (int i = 0; i < CPL; i++) {
+                    tot[i] += acc[i];
+                    acc[i] = 0.0f;
+                }
+            }
             int cj = -1;
             float vj = 0.0f;
             if (kb + lane < K) {
@@ -69,7 +76,9 @@ __global__ __launch_bounds__(kBlock) void k_ell_fast(int64_t R, int64_t K,
             }
             if (m < G) break;
         }
-        store_row_stream<NQ, G>(Y + row * ldy + c0, qok, acc);
+#pragma unroll
+        for (int i = 0; i < CPL; i++) tot[i] += acc[i];
+        store_row_stream<NQ, G>(Y + row * ldy + c0, qok, tot);
     }
 }
 
@@ -95,10 +104,17 @@ __global__ __launch_bounds__(kBlock) void k_dia_fast(int64_t R, int64_t C, int64
     for (int64_t tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
         const int64_t row = tile * GPB + g;
         if (row >= R) break;
-        float acc[CPL];
+        float acc[CPL], tot[CPL];
 #pragma unroll
-        for (int i = 0; i < CPL; i++) acc[i] = 0.0f;
+        for (int i = 0; i < CPL; i++) acc[i] = tot[i] = 0.0f;
         for (int64_t db = 0; db < ND; db += G) {
+            if (db > 0 && db % kChainFold == 0) {  // fold the running chain every kChainFold diagonals
+#pragma unroll
+                for (int i = 0; i < CPL; i++) {
+                    tot[i] += acc[i];
+                    acc[i] = 0.0f;
+                }
+            }
             int cj = 0;
             float vj = 0.0f;
             bool ok = false;
@@ -126,7 +142,9 @@ __global__ __launch_bounds__(kBlock) void k_dia_fast(int64_t R, int64_t C, int64
                     gather_batch<U, NQ, G, true>(cc, vv, j, m, X, ldx, c0, qok, acc);
             }
         }
-        store_row_stream<NQ, G>(Y + row * ldy + c0, qok, acc);
+#pragma unroll
+        for (int i = 0; i < CPL; i++) tot[i] += acc[i];
+        store_row_stream<NQ, G>(Y + row * ldy + c0, qok, tot);
     }
 }
 

@@ -1,6 +1,6 @@
 """Profile the training matrices on the GPU: features + per-format SpMM time.
 
-Usage: python -m paper_2111_00352_amd.selector.collect OUT.csv [--random N] [--structured M]
+Usage: python -m paper_2111_00352_amd.selector.collect OUT.csv [--random N] [--structured M] [--eval E]
 
 Each (matrix, F) row holds the Table 2 features (Sec. 4.4), the 16x16 block
 count, F, and the median time of every storage format measured by the
@@ -47,6 +47,8 @@ def main():
     ap.add_argument("out")
     ap.add_argument("--random", type=int, default=300)
     ap.add_argument("--structured", type=int, default=160)
+    ap.add_argument("--eval", type=int, default=0,
+                    help="held-out matrices with random float values (graphgen.evaluation_matrix)")
     ap.add_argument("--reps", type=int, default=5)
     ap.add_argument("--start", type=int, default=0, help="first job (to split a collection)")
     ap.add_argument("--count", type=int, default=None, help="number of jobs from --start")
@@ -54,14 +56,16 @@ def main():
     torch.cuda.set_device(0)
     jobs = [("random", i, (64, 128)) for i in range(a.random)]
     jobs += [("structured", i, (64, 128, 256)) for i in range(a.structured)]
+    jobs += [("eval", i, (64, 128)) for i in range(a.eval)]
     jobs = jobs[a.start:None if a.count is None else a.start + a.count]
     t0 = time.time()
     with open(a.out, "w", newline="") as fh:
         w = csv.writer(fh)
         w.writerow(HEADER)
         for k, (kind, i, Fs) in enumerate(jobs):
-            n, row, col, val, meta = (graphgen.training_matrix(i) if kind == "random"
-                                      else graphgen.structured_matrix(i))
+            gen = {"random": graphgen.training_matrix, "structured": graphgen.structured_matrix,
+                   "eval": graphgen.evaluation_matrix}[kind]
+            n, row, col, val, meta = gen(i)
             for F in Fs:
                 feats, times = profile(n, row, col, val, F, k, a.reps)
                 w.writerow([kind, i, meta["kind"], n, row.size, F] + feats["f"] + [feats["n_blocks16"]]

@@ -1,6 +1,8 @@
 """Train the format predictor from profiled data and export it.
 
 Usage: python -m paper_2111_00352_amd.selector.train [DATA.csv] [--out model.gsm]
+           [--eval-csv eval.csv --eval-md generalisation.md] | [--importance importance.md] |
+           [--w-sweep 0,0.25,... --md w_sweep.md]
 
 Labels follow Eq. 1 with w = 1: the fastest format of each (matrix, F) row,
 formats within 3% counting as tied and resolved in the order CSR < COO < ELL
@@ -240,6 +242,72 @@ def w_sweep(a, X, T, groups, ws):
             fh.write("\n".join(lines) + "\n")
 
 
+INPUT_NAMES = FEATS + ["bsr16_fill", "F"]
+
+
+def importance(a, X, T, groups):
+    """Fig. 7 analogue (Sec. 4.4): the cross-validated accuracy and fraction
+    of the profiling oracle lost when one predictor input is left out, for
+    each of the 21 inputs."""
+    y = labels(T)
+    base = cross_validate(X, y, groups, a.folds)
+    acc0 = float((base == y).mean())
+    frac0 = evaluate(T, base)[1]
+    rows = []
+    for i, name in enumerate(INPUT_NAMES):
+        keep = [j for j in range(X.shape[1]) if j != i]
+        pred = cross_validate(X[:, keep], y, groups, a.folds)
+        acc = float((pred == y).mean())
+        frac = evaluate(T, pred)[1]
+        rows.append((name, acc0 - acc, frac0 - frac))
+        print(f"without {name:12s} accuracy {acc:.3f} ({acc0 - acc:+.3f})  fraction of oracle {frac:.3f}",
+              flush=True)
+    rows.sort(key=lambda r: -r[1])
+    lines = [f"Leave-one-out importance of the predictor's inputs on {len(y)} profiled samples "
+             f"({len(set(groups))} matrices), {a.folds}-fold grouped cross-validation "
+             "(`python -m paper_2111_00352_amd.selector.train --importance ...`): the drop in accuracy "
+             f"and in fraction of the profiling oracle when the input is left out.  With every input: "
+             f"accuracy {acc0:.3f}, fraction of oracle {frac0:.3f}.", "",
+             "| input left out | accuracy drop | fraction-of-oracle drop |", "|---|---|---|"]
+    for name, da, df in rows:
+        lines.append(f"| {name} | {da:+.3f} | {df:+.4f} |")
+    with open(a.importance, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+
+
+def generalisation(a, clf, mn, mx):
+    """The final model on held-out matrices with random float values
+    (Sec. 5.1: generalisation to unseen sizes and sparsity): accuracy against
+    the profiled label, speedup over fixed CSR and fraction of the profiling
+    oracle (Sec. 6.3), overall and by size."""
+    Xe, Te, ge, _ = load(a.eval_csv)
+    ye = labels(Te)
+    pe = clf.predict(normalise(Xe, mn, mx))
+    acc = float((pe == ye).mean())
+    sp, frac, orac, bad = evaluate(Te, pe)
+    print(f"held-out set: {len(ye)} samples, {len(set(ge))} matrices; accuracy {acc:.3f}; speedup over CSR "
+          f"{sp:.3f}x (oracle {orac:.3f}x); fraction of oracle {frac:.3f}; infeasible picks {bad}")
+    n = Xe[:, FEATS.index("numRow")]
+    lines = [f"The shipped model (trained on the profiled training set only) on {len(set(ge))} held-out matrices "
+             f"with random float values, {len(ye)} (matrix, F) samples, profiled on the same kernels "
+             "(`python -m paper_2111_00352_amd.selector.train --eval-csv selector/eval.csv ...`).", "",
+             "| matrices | samples | accuracy | speedup over CSR (geo-mean) | profiling oracle over CSR | "
+             "fraction of oracle | infeasible picks |", "|---|---|---|---|---|---|---|"]
+    lines.append(f"| all | {len(ye)} | {acc:.3f} | {sp:.3f}x | {orac:.3f}x | {frac:.3f} | {bad} |")
+    for lo, hi in ((0, 15001), (15001, 61000)):
+        msk = (n >= lo) & (n < hi)
+        if msk.sum():
+            s2, f2, o2, b2 = evaluate(Te[msk], pe[msk])
+            lab = "n <= 15,000 (training sizes)" if lo == 0 else "n > 15,000 (beyond them)"
+            lines.append(f"| {lab} | {int(msk.sum())} | {float((pe[msk] == ye[msk]).mean()):.3f} | {s2:.3f}x | "
+                         f"{o2:.3f}x | {f2:.3f} | {b2} |")
+    counts = ", ".join(f"{TIE_ORDER[c]} {int((ye == c).sum())}" for c in range(len(TIE_ORDER)))
+    lines += ["", f"Profiled labels: {counts}."]
+    if a.eval_md:
+        with open(a.eval_md, "w") as fh:
+            fh.write("\n".join(lines) + "\n")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("data", nargs="?", default=DATA_PATH)
@@ -248,12 +316,18 @@ def main():
     ap.add_argument("--w-sweep", help="comma-separated w values of Eq. 1: cross-validate a model per w "
                                       "(labels from time and memory) instead of exporting one")
     ap.add_argument("--md", help="with --w-sweep: also write the table as markdown")
+    ap.add_argument("--importance", help="write the leave-one-out input importance table (markdown) "
+                                         "instead of exporting a model")
+    ap.add_argument("--eval-csv", help="held-out profiles: evaluate the exported model on them")
+    ap.add_argument("--eval-md", help="with --eval-csv: write the evaluation table (markdown)")
     a = ap.parse_args()
     from sklearn.model_selection import GroupKFold
 
     X, T, groups, kinds = load(a.data)
     if a.w_sweep:
         return w_sweep(a, X, T, groups, [float(v) for v in a.w_sweep.split(",")])
+    if a.importance:
+        return importance(a, X, T, groups)
     y = labels(T)
     print(f"{len(y)} samples, {len(set(groups))} matrices; label counts: "
           + ", ".join(f"{TIE_ORDER[c]}={int((y == c).sum())}" for c in range(5)))
@@ -283,6 +357,8 @@ def main():
     print(f"exported {len(trees)} trees to {a.out}; agreement with scikit-learn {agree:.4f}")
     if agree < 1.0:
         sys.exit("exported model disagrees with scikit-learn")
+    if a.eval_csv:
+        generalisation(a, clf, mn, mx)
 
 
 if __name__ == "__main__":

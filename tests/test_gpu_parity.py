@@ -198,6 +198,39 @@ def test_long_and_dense_rows(fmt):
     check_spmm(case, m, X)
 
 
+def _uniform_long_rows(R, C, lo, hi, seed, hubs=()):
+    # every row holds lo..hi entries at uniformly drawn columns, plus dense hub rows
+    rng = np.random.default_rng(seed)
+    keys = []
+    for r in range(R):
+        n = C if r in hubs else int(rng.integers(lo, hi + 1))
+        keys.append(r * C + np.sort(rng.choice(C, size=n, replace=False)).astype(np.int64))
+    keys = np.concatenate(keys)
+    row, col = (keys // C).astype(np.int32), (keys % C).astype(np.int32)
+    val = rng.standard_normal(row.size).astype(np.float32)
+    val[val == 0] = 0.5
+    return Case(R, C, row, col, val)
+
+
+@pytest.mark.parametrize("group_row", ["", "128", "300"])
+@pytest.mark.parametrize("sort", ["1", "2"])
+def test_csr_group_tier(monkeypatch, group_row, sort):
+    # more medium rows (129..1024 entries) than resident workgroups: rows up
+    # to the group limit take one lane group each and are summed chunk by
+    # chunk; longer rows (hubs of 6,000) are cut into chunk items.  128 gives
+    # the chunk-items-only plan, 300 a limit between the row lengths.
+    if group_row:
+        monkeypatch.setenv("GS_CSR_GROUP_ROW", group_row)
+    monkeypatch.setenv("GS_CSR_GROUP_MIN", "1000")  # the tier's default needs 8 medium rows per resident workgroup
+    monkeypatch.setenv("GS_CSR_SORT", sort)
+    case = _uniform_long_rows(2600, 6000, 150, 700, 95, hubs=(0, 1300, 2599))
+    m = case.build("csr")
+    for F, seed in ((64, 96), (36, 97), (132, 98)):
+        check_spmm(case, m, graphgen.features_x(case.C, F, seed, "normal"))
+    for fmt in ("ell", "dia", "bsr", "coo"):  # the same long rows through the folded chains of every format
+        check_spmm(case, case.build(fmt), graphgen.features_x(case.C, 64, 99, "normal"))
+
+
 @pytest.mark.parametrize("cpl", ["", "4", "16"])
 @pytest.mark.parametrize("ranges", ["", "1", "3", "50", "997"])
 def test_coo_ranges_split_rows(monkeypatch, ranges, cpl):
