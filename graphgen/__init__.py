@@ -380,6 +380,28 @@ def training_matrix(i: int):
     return n, row, col, np.ones(row.size, np.float32), dict(kind="random01", density=d)
 
 
+LARGE_SIZE_RANGE = (15000, 60000)
+
+
+def large_training_matrix(i: int):
+    """Large training matrix i (0..99): random 0/1, n log-uniform in
+    15,000..60,000 (GNN graph sizes, above the paper's 15,000), density
+    log-uniform in 0.01%..10% (nnz capped at 30M).  Disjoint seeds from the
+    evaluation matrices."""
+    rng = _rng(80_000 + i)
+    lo, hi = LARGE_SIZE_RANGE
+    n = int(round(float(np.exp(rng.uniform(np.log(lo), np.log(hi))))))
+    d = float(np.exp(rng.uniform(np.log(1e-4), np.log(0.1))))
+    d = min(d, TRAIN_NNZ_CAP / float(n * n))
+    if d > 0.02:
+        row, col = _bernoulli_rows(rng, n, d)
+    else:
+        k = max(1, int(rng.binomial(n * n, d)))
+        keys = np.unique(rng.integers(0, n * n, size=k, dtype=np.int64))
+        row, col = (keys // n).astype(np.int32), (keys % n).astype(np.int32)
+    return n, row, col, np.ones(row.size, np.float32), dict(kind="random01-large", density=d)
+
+
 EVAL_SIZE_RANGE = (1000, 60000)
 
 

@@ -1,6 +1,6 @@
 """Profile the training matrices on the GPU: features + per-format SpMM time.
 
-Usage: python -m paper_2111_00352_amd.selector.collect OUT.csv [--random N] [--structured M] [--eval E]
+Usage: python -m paper_2111_00352_amd.selector.collect OUT.csv [--random N] [--structured M] [--large L] [--eval E]
 
 Each (matrix, F) row holds the Table 2 features (Sec. 4.4), the 16x16 block
 count, F, and the median time of every storage format measured by the
@@ -47,6 +47,8 @@ def main():
     ap.add_argument("out")
     ap.add_argument("--random", type=int, default=300)
     ap.add_argument("--structured", type=int, default=160)
+    ap.add_argument("--large", type=int, default=100,
+                    help="random 0/1 matrices of 15,000..60,000 rows (graphgen.large_training_matrix)")
     ap.add_argument("--eval", type=int, default=0,
                     help="held-out matrices with random float values (graphgen.evaluation_matrix)")
     ap.add_argument("--reps", type=int, default=5)
@@ -56,6 +58,7 @@ def main():
     torch.cuda.set_device(0)
     jobs = [("random", i, (64, 128)) for i in range(a.random)]
     jobs += [("structured", i, (64, 128, 256)) for i in range(a.structured)]
+    jobs += [("large", i, (64, 128)) for i in range(a.large)]
     jobs += [("eval", i, (64, 128)) for i in range(a.eval)]
     jobs = jobs[a.start:None if a.count is None else a.start + a.count]
     t0 = time.time()
@@ -64,7 +67,7 @@ def main():
         w.writerow(HEADER)
         for k, (kind, i, Fs) in enumerate(jobs):
             gen = {"random": graphgen.training_matrix, "structured": graphgen.structured_matrix,
-                   "eval": graphgen.evaluation_matrix}[kind]
+                   "large": graphgen.large_training_matrix, "eval": graphgen.evaluation_matrix}[kind]
             n, row, col, val, meta = gen(i)
             for F in Fs:
                 feats, times = profile(n, row, col, val, F, k, a.reps)

@@ -73,35 +73,44 @@ def predict_time(model, Xn, reps=200):
     return float(np.median(ts))
 
 
+def compare(data=DATA_PATH, folds=5, timing=True):
+    """Cross-validates every candidate predictor: rows of (name, accuracy,
+    speedup over CSR, fraction of oracle, oracle over CSR, infeasible picks,
+    median one-prediction time in s or None)."""
+    from sklearn.model_selection import GroupKFold
+
+    X, T, groups, kinds = train.load(data)
+    y = train.labels(T)
+    rows = []
+    for name, make in candidates().items():
+        pred = np.zeros_like(y)
+        tpred = []
+        for tr, te in GroupKFold(n_splits=folds).split(X, y, groups):
+            mn, mx = X[tr].min(axis=0), X[tr].max(axis=0)
+            m = make().fit(train.normalise(X[tr], mn, mx), y[tr])
+            Xte = train.normalise(X[te], mn, mx)
+            pred[te] = m.predict(Xte)
+            if timing:
+                tpred.append(predict_time(m, Xte, reps=50))
+        acc = float((pred == y).mean())
+        sp, frac, orac, bad = train.evaluate(T, pred)
+        rows.append((name, acc, sp, frac, orac, bad, float(np.median(tpred)) if timing else None))
+    return rows, len(y), len(set(groups))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("data", nargs="?", default=DATA_PATH)
     ap.add_argument("--folds", type=int, default=5)
     ap.add_argument("--md", help="also write the table as markdown to this file")
     a = ap.parse_args()
-    from sklearn.model_selection import GroupKFold
-
-    X, T, groups, kinds = train.load(a.data)
-    y = train.labels(T)
-    rows = []
-    for name, make in candidates().items():
-        pred = np.zeros_like(y)
-        tpred = []
-        for tr, te in GroupKFold(n_splits=a.folds).split(X, y, groups):
-            mn, mx = X[tr].min(axis=0), X[tr].max(axis=0)
-            m = make().fit(train.normalise(X[tr], mn, mx), y[tr])
-            Xte = train.normalise(X[te], mn, mx)
-            pred[te] = m.predict(Xte)
-            tpred.append(predict_time(m, Xte, reps=50))
-        acc = float((pred == y).mean())
-        sp, frac, orac, bad = train.evaluate(T, pred)
-        rows.append((name, acc, sp, frac, orac, bad, float(np.median(tpred))))
+    rows, n_samples, n_matrices = compare(a.data, a.folds)
+    for name, acc, sp, frac, orac, bad, tp in rows:
         print(f"{name:24s} accuracy {acc:.3f}  speedup over CSR {sp:.3f}x (oracle {orac:.3f}x)  "
-              f"fraction of oracle {frac:.3f}  infeasible picks {bad}  "
-              f"predict {rows[-1][-1] * 1e6:.0f} us", flush=True)
+              f"fraction of oracle {frac:.3f}  infeasible picks {bad}  predict {tp * 1e6:.0f} us", flush=True)
     if a.md:
-        lines = [f"Predictor comparison on {len(y)} profiled (matrix, F) samples from "
-                 f"{len(set(groups))} matrices, {a.folds}-fold grouped cross-validation "
+        lines = [f"Predictor comparison on {n_samples} profiled (matrix, F) samples from "
+                 f"{n_matrices} matrices, {a.folds}-fold grouped cross-validation "
                  "(`python -m paper_2111_00352_amd.selector.compare`).", "",
                  "| predictor | accuracy | speedup over CSR (geo-mean) | fraction of oracle | "
                  "infeasible picks | one prediction (scikit-learn, host) |",

@@ -819,19 +819,23 @@ def test_library_predictor_matches_the_training_code():
 
 
 def test_trained_model_choice_is_near_the_profiled_best():
-    # the shipped ensemble against the exhaustive selector on unseen inputs
+    # the shipped ensemble against the exhaustive selector (the paper's
+    # oracle, Sec. 6.3) on inputs it was not trained on: the five scaled
+    # workloads at their own widths.  The chosen format's time over the
+    # fastest one's, geometric mean at least 0.9 and none below 0.75.
     ratios = []
-    for k in (2, 3, 4):
+    for k in (1, 2, 3, 4, 5):
         g = graphgen.scaled(k)
         case = _case_from_graph(g)
         X = _dev(g.X)
         shape = (case.R, case.C)
-        prof = gs.SelectContext("profile", profile_reps=5)
+        prof = gs.SelectContext("profile", profile_reps=10)
         prof.run(1, case.d_row, case.d_col, case.d_val, shape, X)
         times = {f: t for f, t in prof.stats()["scores"].items() if t > 0}
         chosen = gs.SelectContext("model").select(1, case.d_row, case.d_col, case.d_val, shape, g.F)
         ratios.append(min(times.values()) / times[chosen])
-    assert np.exp(np.mean(np.log(ratios))) > 0.6, ratios
+    assert np.exp(np.mean(np.log(ratios))) >= 0.9, ratios
+    assert min(ratios) >= 0.75, ratios
 
 
 @pytest.mark.parametrize("path", ["lds", "global"])
