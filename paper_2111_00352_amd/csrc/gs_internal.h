@@ -134,12 +134,17 @@ struct gs_matrix_ {
     int64_t n_medium_rows = 0, n_medium_chunks = 0;  // long rows of at most csr_wg_thr entries
     int csr_wg_thr = 0;
     bool csr_sorted = false; // items ordered by decreasing length
+    bool csr_grouped = false; // group tier: short items may be rows of up to kCsrGroupRow entries
     bool csr_planned = false; // plan_csr has run (a CSR built only for its features has no plan)
     // CSR: column indices tagged with their column's reference class (bit
-    // length of its entry count) in bits 27..30, and the number of columns
-    // in each class; empty when the gathers do not use classes
-    gs::DevBuf csr_colf;
+    // length of its entry count) in bits 27..30 (made by the first SpMM that
+    // gathers by class), each column's class, and the number of columns in
+    // each class; empty when the matrix does not use classes
+    gs::DevBuf csr_colf, col_cls;  // col_cls: one byte per column, its class
     int64_t col_class_cols[16] = {};
+    // CSR: entry counts of the columns, left by feature extraction for the
+    // plan (which frees them)
+    gs::DevBuf col_counts;
     // CSR: entries inside their row tile's window, per candidate tile of 32,
     // 64, 128 and 256 rows with halo 0 / 1 (natural-order matrices without
     // long rows only; win_counted says whether they were counted)
@@ -272,7 +277,8 @@ void count_blocks_async(const gs_matrix_ &csr, int b, unsigned long long *total,
 
 // --------------------------------------------------- features (gs_features)
 
-void features_from_csr(const gs_matrix_ &csr, hipStream_t s, gs_features *out);
+// Keeps the column counts in csr.col_counts when csr has no work plan yet.
+void features_from_csr(gs_matrix_ &csr, hipStream_t s, gs_features *out);
 // Entry counts cc[0..C) of the columns of col[0..Z) (cc is cleared here).
 void column_counts(const int32_t *col, int64_t C, int64_t Z, int32_t *cc, hipStream_t s);
 // Diagonal occupancy bitmap of a CSR matrix: bit (col - row + R - 1) of

@@ -205,17 +205,28 @@ __global__ __launch_bounds__(kBlock) void k_bsr16_hybrid(
     for (int64_t u = xcd_tile(blockIdx.x, gridDim.x); u < units; u += gridDim.x) {
         const int64_t br = u * 4 + wave;
         if (br >= nbr) break;
-        f32x4 acc[T], tot[T];
+        f32x4 acc[T];
 #pragma unroll
-        for (int t = 0; t < T; t++) acc[t] = tot[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int t = 0; t < T; t++) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+        // every kFoldBlocks dense blocks (16 products each) the running sums
+        // are added into the wave's LDS tile, which then holds the total
+        bool folded = false;
+        auto to_tile = [&](bool add) {
+#pragma unroll
+            for (int t = 0; t < T; t++)
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    float &c = tl[(4 * kk + i) * LDT + 16 * t + m];
+                    c = add ? c + acc[t][i] : acc[t][i];
+                }
+        };
         const int64_t d0 = dptr[br], d1 = dptr[br + 1];
         for (int64_t d = d0; d < d1; d += NB) {
-            if (d > d0 && (d - d0) % kFoldBlocks == 0) {  // 16 terms per block into the running chain
+            if (d > d0 && (d - d0) % kFoldBlocks == 0) {
+                to_tile(folded);
+                folded = true;
 #pragma unroll
-                for (int t = 0; t < T; t++) {
-                    tot[t] += acc[t];
-                    acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-                }
+                for (int t = 0; t < T; t++) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
             }
             uint64_t mask[NB];
             int64_t xr0[NB];
@@ -256,12 +267,7 @@ __global__ __launch_bounds__(kBlock) void k_bsr16_hybrid(
         }
         // accumulator layout (lane m + 16 kk: rows 4kk..4kk+3, column m of
         // each tile) -> row-major tile in this wave's LDS rows
-#pragma unroll
-        for (int t = 0; t < T; t++) {
-            tot[t] += acc[t];
-#pragma unroll
-            for (int i = 0; i < 4; i++) tl[(4 * kk + i) * LDT + 16 * t + m] = tot[t][i];
-        }
+        to_tile(folded);
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");

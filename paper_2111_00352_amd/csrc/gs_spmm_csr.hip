@@ -68,7 +68,9 @@ __device__ __forceinline__ void gather_entries(const int32_t *__restrict__ col,
     }
 }
 
-template <int CPL, int G, bool FULL, bool CLS>
+// GROUPED: the plan's group tier is active, so short items may be rows of up
+// to the group limit, summed chunk by chunk (compiled out otherwise).
+template <int CPL, int G, bool FULL, bool CLS, bool GROUPED>
 __global__ __launch_bounds__(kBlock) void k_csr_rows(
     int64_t n_long, const int32_t *__restrict__ long_rows, const int32_t *__restrict__ rp,
     int chunk, int64_t n_short, const int4 *__restrict__ items, const int32_t *__restrict__ col,
@@ -130,7 +132,7 @@ __global__ __launch_bounds__(kBlock) void k_csr_rows(
             const int64_t it = (t - n_long) * GPB + g;
             if (it >= n_short) break;  // later tiles of this workgroup are past the end too
             const int4 d = items[it];
-            if (d.z <= chunk) {
+            if (!GROUPED || d.z <= chunk) {
                 gather_entries<NQ, G, U, CLS>(col, val, d.y, (int64_t)d.y + d.z, X, ldx, c0, qok, acc, lane,
                                               hot_cls);
             } else {  // a row of up to the group limit: chunk by chunk, each summed in fresh registers
@@ -249,18 +251,11 @@ __global__ __launch_bounds__(kBlock) void k_csr_window(
         }
         __syncthreads();
         for (int64_t r = r0 + g; r < r1; r += GPB) {
-            float acc[CPL], tot[CPL];
+            float acc[CPL];  // rows hold at most the short-row limit of entries: one chain
 #pragma unroll
-            for (int i = 0; i < CPL; i++) acc[i] = tot[i] = 0.0f;
+            for (int i = 0; i < CPL; i++) acc[i] = 0.0f;
             const int64_t s = rp[r], e = rp[r + 1];
             for (int64_t kb = s; kb < e; kb += G) {
-                if (kb > s && (kb - s) % kChainFold == 0) {  // fold the running chain
-#pragma unroll
-                    for (int i = 0; i < CPL; i++) {
-                        tot[i] += acc[i];
-                        acc[i] = 0.0f;
-                    }
-                }
                 const int m = (e - kb) < G ? (int)(e - kb) : G;
                 int cj = 0;
                 float vj = 0.0f;
@@ -303,9 +298,7 @@ __global__ __launch_bounds__(kBlock) void k_csr_window(
                     }
                 }
             }
-#pragma unroll
-            for (int i = 0; i < CPL; i++) tot[i] += acc[i];
-            store_row_stream<NQ, G>(Y + r * ldy + c0, qok, tot);
+            store_row_stream<NQ, G>(Y + r * ldy + c0, qok, acc);
         }
     }
 }
@@ -496,13 +489,31 @@ __global__ __launch_bounds__(kBlock) void k_class_hist(const int32_t *__restrict
     if (threadIdx.x < 16 && h[threadIdx.x]) atomicAdd(&hist[threadIdx.x], h[threadIdx.x]);
 }
 
-// Class-tagged copy of the column indices: col | class(count of col) << 27.
-__global__ __launch_bounds__(kBlock) void k_tag_cols(const int32_t *__restrict__ col, int64_t Z,
-                                                     const int32_t *__restrict__ cc, int32_t *__restrict__ tagged)
+// Reference class of every column, one byte each (so that the tagging pass
+// gathers from an array a quarter the size of the counts).
+__global__ __launch_bounds__(kBlock) void k_col_classes(const int32_t *__restrict__ cc, int64_t C,
+                                                        uint8_t *__restrict__ cls)
 {
-    for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < Z; e += (int64_t)gridDim.x * kBlock) {
-        const int c = col[e];
-        tagged[e] = c | (col_class(cc[c]) << kColClassShift);
+    for (int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x; j < C; j += (int64_t)gridDim.x * kBlock)
+        cls[j] = (uint8_t)col_class(cc[j]);
+}
+
+// Class-tagged copy of the column indices: col | class(col) << 27, four
+// entries per thread.
+__global__ __launch_bounds__(kBlock) void k_tag_cols(const int32_t *__restrict__ col, int64_t Z,
+                                                     const uint8_t *__restrict__ cls, int32_t *__restrict__ tagged)
+{
+    for (int64_t e0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * 4; e0 < Z;
+         e0 += (int64_t)gridDim.x * kBlock * 4) {
+        int c[4];
+#pragma unroll
+        for (int u = 0; u < 4; u++) c[u] = e0 + u < Z ? col[e0 + u] : 0;
+        int t[4];
+#pragma unroll
+        for (int u = 0; u < 4; u++) t[u] = (int)cls[c[u]];
+#pragma unroll
+        for (int u = 0; u < 4; u++)
+            if (e0 + u < Z) tagged[e0 + u] = c[u] | (t[u] << kColClassShift);
     }
 }
 
@@ -543,7 +554,7 @@ __global__ __launch_bounds__(kBlock) void k_win_counts(const int32_t *__restrict
 void plan_windows(gs_matrix_ &m, hipStream_t s)
 {
     const char *e = std::getenv("GS_CSR_WINDOW");
-    if ((e && std::string(e) == "off") || m.csr_sorted || m.n_long_rows > 0 || m.Z == 0) return;
+    if ((e && std::string(e) == "off") || m.csr_sorted || m.csr_grouped || m.n_long_rows > 0 || m.Z == 0) return;
     DevBuf cnt;
     cnt.alloc(sizeof(unsigned long long) * 2 * kWinCands, s);
     GS_HIP(hipMemsetAsync(cnt.p, 0, cnt.bytes, s));
@@ -558,25 +569,30 @@ void plan_windows(gs_matrix_ &m, hipStream_t s)
 }
 
 // Reference classes of the columns, for gathers that keep often referenced X
-// rows in L2: counts per column, the number of columns in each class (read
-// back) and the class-tagged column copy.  Built for skewed matrices (rows
-// ordered by length; GS_CSR_HOTCOLD = on / off forces it) whose column count
-// fits the 27-bit column field.
+// rows in the caches: counts per column, each column's class (one byte) and
+// the number of columns in each class (read back).  The class-tagged copy of
+// the column indices is made by the first SpMM that uses the classes.  Built
+// for skewed matrices (rows ordered by length; GS_CSR_HOTCOLD = on / off
+// forces it) whose column count fits the 27-bit column field.
 void plan_col_classes(gs_matrix_ &m, hipStream_t s)
 {
     const char *e = std::getenv("GS_CSR_HOTCOLD");
     const bool on = e && *e ? std::string(e) == "on" : m.csr_sorted;
-    if (!on || m.Z == 0 || m.C > kColMask + 1) return;
-    DevBuf cc, hist;
-    cc.alloc((size_t)m.C * 4, s);
+    if (!on || m.Z == 0 || m.C > kColMask + 1) {
+        m.col_counts.reset();
+        return;
+    }
+    DevBuf cc = std::move(m.col_counts), hist;  // counted by feature extraction, if it ran
+    if (!cc.p) {
+        cc.alloc((size_t)m.C * 4, s);
+        column_counts(m.col.as<int32_t>(), m.C, m.Z, cc.as<int32_t>(), s);
+    }
     hist.alloc(16 * 4, s);
-    column_counts(m.col.as<int32_t>(), m.C, m.Z, cc.as<int32_t>(), s);
     GS_HIP(hipMemsetAsync(hist.p, 0, 16 * 4, s));
     k_class_hist<<<plan_grid(m.C), kBlock, 0, s>>>(cc.as<int32_t>(), m.C, hist.as<int32_t>());
     GS_HIP(hipGetLastError());
-    m.csr_colf.alloc((size_t)m.Z * 4, s);
-    k_tag_cols<<<plan_grid(m.Z), kBlock, 0, s>>>(m.col.as<int32_t>(), m.Z, cc.as<int32_t>(),
-                                                 m.csr_colf.as<int32_t>());
+    m.col_cls.alloc((size_t)m.C, s);
+    k_col_classes<<<plan_grid(m.C), kBlock, 0, s>>>(cc.as<int32_t>(), m.C, m.col_cls.as<uint8_t>());
     GS_HIP(hipGetLastError());
     int32_t h[16];
     GS_HIP(hipMemcpyAsync(h, hist.p, sizeof h, hipMemcpyDeviceToHost, s));
@@ -633,9 +649,11 @@ void plan_csr(gs_matrix_ &m, hipStream_t s)
     int64_t n_long = st.n_long, n_huge = st.n_huge;
     const int64_t n_medium = st.n_long - st.n_huge;
     const int64_t group_min = env_int("GS_CSR_GROUP_MIN", resident_workgroups() * 8);
+    m.csr_grouped = false;
     if (n_medium > group_min && group_max > thr) {
         thr_eff = wg_thr_eff = group_max;
         n_long = n_huge = st.n_group;
+        m.csr_grouped = true;
     } else if (n_medium > resident_workgroups()) {
         wg_thr_eff = thr;
         n_huge = st.n_long;
@@ -725,12 +743,22 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
     // 4 / 32 / 128 / 256 MiB gave 4185 / 3286 / 3231 / 3306 us.  Not used
     // when the rows of every referenced column fit the budget.
     int hot_cls = 0;
-    if (m.csr_colf.p && cpl == 4) {
+    if (m.col_cls.p && cpl == 4) {
         const int64_t budget = (int64_t)env_int("GS_CSR_HOT_KB", 65536) * 1024 / (F * 4);
         int64_t cum = 0;
         for (int c = 15; c >= 1 && !hot_cls; c--) {
             cum += m.col_class_cols[c];
             if (cum > budget) hot_cls = c < 15 ? c + 1 : 15;
+        }
+        if (hot_cls && !m.csr_colf.p) {
+            if (fixed) {
+                hot_cls = 0;  // no allocation allowed: plain gathers
+            } else {          // first use: the class-tagged column copy
+                m.csr_colf.alloc((size_t)m.Z * 4, s);
+                k_tag_cols<<<plan_grid(ceil_div(m.Z, 4)), kBlock, 0, s>>>(
+                    m.col.as<int32_t>(), m.Z, m.col_cls.as<uint8_t>(), m.csr_colf.as<int32_t>());
+                GS_HIP(hipGetLastError());
+            }
         }
     }
     // LDS-staged row tiles: the candidate (tile, halo) that keeps the most
@@ -740,7 +768,7 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
     // tiles of 32 / 64 / 128 rows (32 / 64 / 128 KiB) measured 193 / 280 /
     // 480 us against 209 us without staging.
     int win_T = 0, win_h = 0;
-    if (m.win_counted && m.n_long_rows == 0) {
+    if (m.win_counted && m.n_long_rows == 0 && !m.csr_grouped) {
         const int64_t lds_cap = std::min<int64_t>(max_lds_bytes(), (int64_t)env_int("GS_CSR_WIN_KB", 32) * 1024);
         const int64_t min_in = m.Z * env_int("GS_CSR_WIN_PCT", 50) / 100;
         int64_t best = -1;
@@ -787,21 +815,29 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
         // length-sorted rows, 8 -- about one tile each -- for natural order)
         const int64_t cap = (int64_t)resident_workgroups() * env_int("GS_WG_MULT", m.csr_sorted ? 4 : 8);
         dim3 grid((unsigned)std::max<int64_t>(1, std::min(tiles, cap / slices)), (unsigned)slices);
-        if constexpr (CPL == 4) {
+        auto rows = [&](auto cls_t, auto grp_t, const int32_t *cols) {
+            constexpr bool CL = decltype(cls_t)::value, GR = decltype(grp_t)::value;
+            k_csr_rows<CPL, G, FU, CL, GR><<<grid, kBlock, 0, s>>>(
+                m.n_medium_rows, m.long_rows.as<int32_t>(), m.row_ptr.as<int32_t>(), m.csr_chunk, n_group_items,
+                m.csr_items.as<int4>() + m.n_medium_chunks, cols, m.val.as<float>(), X, ldx, Y, ldy, F, work,
+                hot_cls);
+            GS_HIP(hipGetLastError());
+        };
+        bool done = false;
+        if constexpr (CPL == 4) {  // reference classes: only the length-sorted lane shape
             if (hot_cls) {
-                k_csr_rows<CPL, G, FU, true><<<grid, kBlock, 0, s>>>(
-                    m.n_medium_rows, m.long_rows.as<int32_t>(), m.row_ptr.as<int32_t>(), m.csr_chunk,
-                    n_group_items, m.csr_items.as<int4>() + m.n_medium_chunks, m.csr_colf.as<int32_t>(),
-                    m.val.as<float>(), X, ldx, Y, ldy, F, work, hot_cls);
-                GS_HIP(hipGetLastError());
+                if (m.csr_grouped)
+                    rows(std::true_type{}, std::true_type{}, m.csr_colf.as<int32_t>());
+                else
+                    rows(std::true_type{}, std::false_type{}, m.csr_colf.as<int32_t>());
+                done = true;
             }
         }
-        if (!(CPL == 4 && hot_cls)) {
-            k_csr_rows<CPL, G, FU, false><<<grid, kBlock, 0, s>>>(
-                m.n_medium_rows, m.long_rows.as<int32_t>(), m.row_ptr.as<int32_t>(), m.csr_chunk,
-                n_group_items, m.csr_items.as<int4>() + m.n_medium_chunks, m.col.as<int32_t>(),
-                m.val.as<float>(), X, ldx, Y, ldy, F, work, 0);
-            GS_HIP(hipGetLastError());
+        if (!done) {
+            if (m.csr_grouped)
+                rows(std::false_type{}, std::true_type{}, m.col.as<int32_t>());
+            else
+                rows(std::false_type{}, std::false_type{}, m.col.as<int32_t>());
         }
         if (n_huge) {
             dim3 g2((unsigned)ceil_div(n_huge, GPB), (unsigned)slices);

@@ -25,7 +25,9 @@ namespace {
 
 constexpr int kBlock = 256;
 
-template <int CPL, int G, bool FULL>
+// FOLD: rows may hold more than kChainFold slots; their running sum is then
+// added into a total every kChainFold slots (compiled out otherwise).
+template <int CPL, int G, bool FULL, bool FOLD>
 __global__ __launch_bounds__(kBlock) void k_ell_fast(int64_t R, int64_t K,
                                                      const int32_t *__restrict__ ec,
                                                      const float *__restrict__ ev,
@@ -47,11 +49,15 @@ __global__ __launch_bounds__(kBlock) void k_ell_fast(int64_t R, int64_t K,
     for (int64_t tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
         const int64_t row = tile * GPB + g;
         if (row >= R) break;
-        float acc[CPL], tot[CPL];
+        float acc[CPL], tot[FOLD ? CPL : 1];
 #pragma unroll
-        for (int i = 0; i < CPL; i++) acc[i] = tot[i] = 0.0f;
+        for (int i = 0; i < CPL; i++) acc[i] = 0.0f;
+        if constexpr (FOLD) {
+#pragma unroll
+            for (int i = 0; i < CPL; i++) tot[i] = 0.0f;
+        }
         for (int64_t kb = 0; kb < K; kb += G) {
-            if (kb > 0 && kb % kChainFold == 0) {  // fold the running chain every kChainFold slots
+            if (FOLD && kb > 0 && kb % kChainFold == 0) {  // fold the running chain every kChainFold slots
 #pragma unroll
                 for (int i = 0; i < CPL; i++) {
                     tot[i] += acc[i];
@@ -76,13 +82,17 @@ __global__ __launch_bounds__(kBlock) void k_ell_fast(int64_t R, int64_t K,
             }
             if (m < G) break;
         }
+        if constexpr (FOLD) {
 #pragma unroll
-        for (int i = 0; i < CPL; i++) tot[i] += acc[i];
-        store_row_stream<NQ, G>(Y + row * ldy + c0, qok, tot);
+            for (int i = 0; i < CPL; i++) acc[i] += tot[i];
+        }
+        store_row_stream<NQ, G>(Y + row * ldy + c0, qok, acc);
     }
 }
 
-template <int CPL, int G, bool FULL>
+// FOLD: more than kChainFold diagonals (the running sum of a row is added
+// into a total every kChainFold diagonals; compiled out otherwise).
+template <int CPL, int G, bool FULL, bool FOLD>
 __global__ __launch_bounds__(kBlock) void k_dia_fast(int64_t R, int64_t C, int64_t ND,
                                                      const int32_t *__restrict__ offsets,
                                                      const float *__restrict__ data,
@@ -104,11 +114,15 @@ __global__ __launch_bounds__(kBlock) void k_dia_fast(int64_t R, int64_t C, int64
     for (int64_t tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
         const int64_t row = tile * GPB + g;
         if (row >= R) break;
-        float acc[CPL], tot[CPL];
+        float acc[CPL], tot[FOLD ? CPL : 1];
 #pragma unroll
-        for (int i = 0; i < CPL; i++) acc[i] = tot[i] = 0.0f;
+        for (int i = 0; i < CPL; i++) acc[i] = 0.0f;
+        if constexpr (FOLD) {
+#pragma unroll
+            for (int i = 0; i < CPL; i++) tot[i] = 0.0f;
+        }
         for (int64_t db = 0; db < ND; db += G) {
-            if (db > 0 && db % kChainFold == 0) {  // fold the running chain every kChainFold diagonals
+            if (FOLD && db > 0 && db % kChainFold == 0) {  // fold the running chain every kChainFold diagonals
 #pragma unroll
                 for (int i = 0; i < CPL; i++) {
                     tot[i] += acc[i];
@@ -142,9 +156,11 @@ __global__ __launch_bounds__(kBlock) void k_dia_fast(int64_t R, int64_t C, int64
                     gather_batch<U, NQ, G, true>(cc, vv, j, m, X, ldx, c0, qok, acc);
             }
         }
+        if constexpr (FOLD) {
 #pragma unroll
-        for (int i = 0; i < CPL; i++) tot[i] += acc[i];
-        store_row_stream<NQ, G>(Y + row * ldy + c0, qok, tot);
+            for (int i = 0; i < CPL; i++) acc[i] += tot[i];
+        }
+        store_row_stream<NQ, G>(Y + row * ldy + c0, qok, acc);
     }
 }
 
@@ -220,8 +236,12 @@ bool spmm_ell_fast(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
         constexpr bool FU = decltype(f_t)::value;
         const int64_t tiles = ceil_div(m.R, kBlock / G);
         dim3 grid(persistent_grid(tiles, sh.slices), (unsigned)sh.slices);
-        k_ell_fast<CPL, G, FU><<<grid, kBlock, 0, s>>>(m.R, m.K, m.ell_col.as<int32_t>(),
-                                                        m.ell_val.as<float>(), X, ldx, Y, ldy, F);
+        if (m.K > kChainFold)
+            k_ell_fast<CPL, G, FU, true><<<grid, kBlock, 0, s>>>(m.R, m.K, m.ell_col.as<int32_t>(),
+                                                                  m.ell_val.as<float>(), X, ldx, Y, ldy, F);
+        else
+            k_ell_fast<CPL, G, FU, false><<<grid, kBlock, 0, s>>>(m.R, m.K, m.ell_col.as<int32_t>(),
+                                                                   m.ell_val.as<float>(), X, ldx, Y, ldy, F);
         GS_HIP(hipGetLastError());
     });
 }
@@ -236,8 +256,12 @@ bool spmm_dia_fast(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
         constexpr bool FU = decltype(f_t)::value;
         const int64_t tiles = ceil_div(m.R, kBlock / G);
         dim3 grid(persistent_grid(tiles, sh.slices), (unsigned)sh.slices);
-        k_dia_fast<CPL, G, FU><<<grid, kBlock, 0, s>>>(m.R, m.C, m.ND, m.offsets.as<int32_t>(),
-                                                        m.dia.as<float>(), X, ldx, Y, ldy, F);
+        if (m.ND > kChainFold)
+            k_dia_fast<CPL, G, FU, true><<<grid, kBlock, 0, s>>>(m.R, m.C, m.ND, m.offsets.as<int32_t>(),
+                                                                  m.dia.as<float>(), X, ldx, Y, ldy, F);
+        else
+            k_dia_fast<CPL, G, FU, false><<<grid, kBlock, 0, s>>>(m.R, m.C, m.ND, m.offsets.as<int32_t>(),
+                                                                   m.dia.as<float>(), X, ldx, Y, ldy, F);
         GS_HIP(hipGetLastError());
     });
 }

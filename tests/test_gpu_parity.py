@@ -838,22 +838,28 @@ def test_trained_model_choice_is_near_the_profiled_best():
     assert min(ratios) >= 0.75, ratios
 
 
-@pytest.mark.parametrize("path", ["lds", "global"])
+@pytest.mark.parametrize("path", ["lds", "global", "windows1", "windows64"])
 def test_diagonal_bitmap_paths_agree(monkeypatch, path):
-    # the per-workgroup LDS bitmap and the global-atomic bitmap must give the
-    # same diagonal set (features N_diags and the DIA layout)
+    # the per-workgroup LDS bitmap, the global-atomic bitmap and the bitmap in
+    # LDS windows (forced here to windows of 1 and 64 words, many per matrix)
+    # must give the same diagonal set (features N_diags and the DIA layout)
     if path == "global":
         monkeypatch.setenv("GS_DIAG_GLOBAL", "1")
+    if path.startswith("windows"):
+        monkeypatch.setenv("GS_DIAG_WIN_WORDS", path[len("windows"):])
     for case in (_random_case(3001, 2500, 20000, 91), _random_case(300, 7000, 9000, 92, empty=0.3),
                  _case_from_graph(graphgen.scaled(3), shuffle_seed=93)):
         check_features(case)
         check_layout(case, "dia")
 
 
-def test_wide_diagonal_bitmap():
-    # a span of 1.6 million diagonals and 700,001 rows is too wide for the
-    # per-workgroup LDS bitmap, so the global-atomic path runs by itself,
-    # with each wave's batches of entries in flight
+@pytest.mark.parametrize("path", ["windows", "global"])
+def test_wide_diagonal_bitmap(monkeypatch, path):
+    # a span of 1.6 million diagonals and 700,001 rows is too wide for one
+    # LDS bitmap: it is marked in LDS windows of the bitmap (default) or with
+    # global atomics, each wave's batches of entries in flight
+    if path == "global":
+        monkeypatch.setenv("GS_DIAG_GLOBAL", "1")
     check_features(_random_case(700_001, 900_000, 1_100_000, 96, empty=0.1))
 
 
