@@ -39,7 +39,7 @@ constexpr int kColMask = (1 << kColClassShift) - 1;
 //
 // CLS: cj holds class-tagged column words; rows of columns whose class is
 // below hot_cls are gathered non-temporally.
-template <int B, int NQ, int G, bool MASKED, bool CLS = false>
+template <int B, int NQ, int G, bool MASKED, bool CLS = false, bool FENCE = false>
 __device__ __forceinline__ void gather_batch(int cj, float vj, int j, int m,
                                              const float *__restrict__ X, int64_t ldx, int64_t c0,
                                              const bool *qok, float *acc, int hot_cls = 0)
@@ -62,6 +62,11 @@ __device__ __forceinline__ void gather_batch(int cj, float vj, int j, int m,
                 x[u][q] = qok[q] ? load_x4(xp + 4 * G * q) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     }
+    // FENCE: every load of the batch is issued before the first use.  Where
+    // the scheduler aims at a higher occupancy it may otherwise sink each
+    // load next to its use, one round trip per X row (seen in the ELL kernel
+    // with chain folds: 50 VGPRs and twice the time on a power-law matrix).
+    if constexpr (FENCE) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < B; u++) {
         const bool live = !MASKED || j + u < m;

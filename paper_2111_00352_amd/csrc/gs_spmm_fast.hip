@@ -56,14 +56,13 @@ __global__ __launch_bounds__(kBlock) void k_ell_fast(int64_t R, int64_t K,
 #pragma unroll
             for (int i = 0; i < CPL; i++) tot[i] = 0.0f;
         }
-        for (int64_t kb = 0; kb < K; kb += G) {
-            if (FOLD && kb > 0 && kb % kChainFold == 0) {  // fold the running chain every kChainFold slots
-#pragma unroll
-                for (int i = 0; i < CPL; i++) {
-                    tot[i] += acc[i];
-                    acc[i] = 0.0f;
-                }
-            }
+        // chains of kChainFold slots (one chain of K without FOLD; kChainFold
+        // is a multiple of G), each added into the total when it ends
+        const int64_t span = FOLD ? kChainFold : K;
+        bool more = true;
+        for (int64_t kc = 0; kc < K && more; kc += span) {
+          const int64_t kend = kc + span < K ? kc + span : K;
+          for (int64_t kb = kc; kb < kend; kb += G) {
             int cj = -1;
             float vj = 0.0f;
             if (kb + lane < K) {
@@ -73,18 +72,29 @@ __global__ __launch_bounds__(kBlock) void k_ell_fast(int64_t R, int64_t K,
             const int m = __popcll((__ballot(cj >= 0) >> gbase) & gmask);
             if (cj < 0) cj = 0;  // padding lanes gather row 0 and are masked
             int j = 0;
-            for (; j + U <= m; j += U) gather_batch<U, NQ, G, false>(cj, vj, j, m, X, ldx, c0, qok, acc);
+            for (; j + U <= m; j += U) gather_batch<U, NQ, G, false, false, FOLD>(cj, vj, j, m, X, ldx, c0, qok, acc);
             if (j < m) {
                 if (U > 1 && m - j <= U / 2)
-                    gather_batch<(U > 1 ? U / 2 : 1), NQ, G, true>(cj, vj, j, m, X, ldx, c0, qok, acc);
+                    gather_batch<(U > 1 ? U / 2 : 1), NQ, G, true, false, FOLD>(cj, vj, j, m, X, ldx, c0, qok, acc);
                 else
-                    gather_batch<U, NQ, G, true>(cj, vj, j, m, X, ldx, c0, qok, acc);
+                    gather_batch<U, NQ, G, true, false, FOLD>(cj, vj, j, m, X, ldx, c0, qok, acc);
             }
-            if (m < G) break;
+            if (m < G) {  // padding reached: the row has no more slots
+                more = false;
+                break;
+            }
+          }
+          if constexpr (FOLD) {
+#pragma unroll
+            for (int i = 0; i < CPL; i++) {
+                tot[i] += acc[i];
+                acc[i] = 0.0f;
+            }
+          }
         }
         if constexpr (FOLD) {
 #pragma unroll
-            for (int i = 0; i < CPL; i++) acc[i] += tot[i];
+            for (int i = 0; i < CPL; i++) acc[i] = tot[i];
         }
         store_row_stream<NQ, G>(Y + row * ldy + c0, qok, acc);
     }
@@ -148,12 +158,12 @@ __global__ __launch_bounds__(kBlock) void k_dia_fast(int64_t R, int64_t C, int64
             const int cc = __shfl(cj, pick, G);
             const float vv = __shfl(vj, pick, G);
             int j = 0;
-            for (; j + U <= m; j += U) gather_batch<U, NQ, G, false>(cc, vv, j, m, X, ldx, c0, qok, acc);
+            for (; j + U <= m; j += U) gather_batch<U, NQ, G, false, false, FOLD>(cc, vv, j, m, X, ldx, c0, qok, acc);
             if (j < m) {
                 if (U > 1 && m - j <= U / 2)
-                    gather_batch<(U > 1 ? U / 2 : 1), NQ, G, true>(cc, vv, j, m, X, ldx, c0, qok, acc);
+                    gather_batch<(U > 1 ? U / 2 : 1), NQ, G, true, false, FOLD>(cc, vv, j, m, X, ldx, c0, qok, acc);
                 else
-                    gather_batch<U, NQ, G, true>(cc, vv, j, m, X, ldx, c0, qok, acc);
+                    gather_batch<U, NQ, G, true, false, FOLD>(cc, vv, j, m, X, ldx, c0, qok, acc);
             }
         }
         if constexpr (FOLD) {
