@@ -282,6 +282,61 @@ def gather_ceiling(gs, dev, stream, reps=10):
     return {"rows": R, "entries_per_row": d, "F": F, "table": rows}
 
 
+def column_panels(gs, g, dev, stream, parts, reps=10):
+    """Column-panel (2-D) schedule of the CSR SpMM: A's columns are cut into
+    P equal ranges, one CSR handle per panel, and the panels run one after
+    another, each gathering only its slice of X (1/P of it, so that for large
+    P the slice fits the memory-side cache or one XCD's L2).  Pass p writes
+    A_p X_p into a Y of its own; Y is their sum in panel order.  Reports the
+    median time of the P passes alone (a lower bound for any accumulating
+    schedule, which must also re-read Y) and with the summation."""
+    import torch
+
+    R, C, Z, F = g.R, g.C, g.nnz, g.F
+    row, col, val = (torch.from_numpy(a).to(dev) for a in (g.row, g.col, g.val))
+    X = torch.from_numpy(g.X).to(dev)
+    whole = gs.build_format(row, col, val, (R, C), "csr")
+    Yref = whole.spmm(X)
+    whole.close()
+    out = []
+    for P in parts:
+        bounds = [C * p // P for p in range(P + 1)]
+        mats = []
+        for p in range(P):
+            c0, c1 = bounds[p], bounds[p + 1]
+            sel = (col >= c0) & (col < c1)
+            m = gs.build_format(row[sel], col[sel] - c0, val[sel], (R, c1 - c0), "csr")
+            mats.append((m, c0, c1, int(sel.sum().item())))
+        Ys = [torch.empty((R, F), dtype=torch.float32, device=dev) for _ in range(P)]
+        Y = torch.empty((R, F), dtype=torch.float32, device=dev)
+
+        def passes(_):
+            for (m, c0, c1, _z), y in zip(mats, Ys):
+                m.spmm(X[c0:c1], out=y)
+
+        def combine(_):
+            Y.copy_(Ys[0])
+            for y in Ys[1:]:
+                Y.add_(y)
+
+        for _ in range(2):
+            passes(None)
+            combine(None)
+        dp, dc = event_durations([passes, combine], stream, reps, [None])
+        err = float(((Y - Yref).abs().max() / Yref.abs().max().clamp_min(1e-30)).item())
+        tp, tc = float(np.median(dp)), float(np.median(dc))
+        out.append({"panels": P, "x_slice_mib": round(C / P * F * 4 / 2**20, 1),
+                    "entries_per_panel": [z for (_m, _a, _b, z) in mats],
+                    "passes_us": round(tp * 1e6, 1), "passes_plus_sum_us": round((tp + tc) * 1e6, 1),
+                    "max_rel_diff_vs_whole": err})
+        log(f"column panels P={P}: {out[-1]['passes_us']} us passes, {out[-1]['passes_plus_sum_us']} us with the sum")
+        for m, *_ in mats:
+            m.close()
+        del mats, Ys, Y
+        torch.cuda.empty_cache()
+    return {"n": R, "nnz": Z, "F": F, "table": out}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -299,6 +354,9 @@ def main():
     ap.add_argument("--gcn-epochs", type=int, default=10)
     ap.add_argument("--gather-ceiling", action="store_true",
                     help="only the random-gather ceiling table of the CSR kernel (X of 2 MiB .. 1 GiB)")
+    ap.add_argument("--column-panels", default=None,
+                    help="only the column-panel schedule table of the CSR SpMM on --config: "
+                         "comma-separated panel counts, e.g. 1,2,4,8,16")
     ap.add_argument("--format", default=None,
                     help="time this format (fixed selector) instead of the predicted one, for profiling")
     ap.add_argument("--profile-run", action="store_true",
@@ -325,6 +383,17 @@ def main():
         return
     k = args.config
     two_layer = k == 5
+    if args.column_panels:
+        g = graphgen.config(k)
+        parts = [int(x) for x in args.column_panels.split(",") if x]
+        res = column_panels(gs, g, dev, stream, parts, reps=max(args.format_reps // 2, 10))
+        res["workload"] = WORKLOADS[k]
+        # plain elementwise copy of known size: calibrates the byte counters
+        src = torch.ones(64 * 2**20, dtype=torch.float32, device=dev)
+        torch.neg(src, out=torch.empty_like(src))
+        torch.cuda.synchronize()
+        print(json.dumps({"column_panels": res}), flush=True)
+        return
 
     t_gen = time.perf_counter()
     g = graphgen.config(k)

@@ -682,6 +682,31 @@ def test_csr_lds_window_tiles(monkeypatch, T, h):
         check_spmm(case, m, graphgen.features_x(C, 132, seed + 6, "normal"))
 
 
+@pytest.mark.parametrize("P", [2, 5])
+def test_column_panel_schedule_sums_to_the_product(P):
+    # the column-panel schedule that bench.py --column-panels measures: one
+    # CSR handle per column range, passes summed in panel order.  Rows are cut
+    # across panels, and the first panel holds no entry.
+    R, C = 1500, 2000
+    row, col, val = graphgen.random_coo(R, C, 24000, 91, empty_rows=0.1)
+    bounds = [C * p // P for p in range(P + 1)]
+    keep = col >= bounds[1]
+    case = Case(R, C, row[keep], col[keep], val[keep])
+    X = graphgen.features_x(C, 64, 92, "normal")
+    Xd = _dev(X)
+    Y = torch.zeros((R, 64), dtype=torch.float32, device=DEV)
+    for p in range(P):
+        c0, c1 = bounds[p], bounds[p + 1]
+        sel = (case.d_col >= c0) & (case.d_col < c1)
+        assert p > 0 or int(sel.sum()) == 0
+        m = gs.build_format(case.d_row[sel], case.d_col[sel] - c0, case.d_val[sel], (R, c1 - c0), "csr")
+        Y += m.spmm(Xd[c0:c1])
+        m.close()
+    Yref, M = oracle.spmm(R, case.rp, case.ccol, case.cval, X)
+    ok, worst = oracle.check_spmm(_host(Y), Yref, M)
+    assert ok, f"panels: worst |err|/bound = {worst}"
+
+
 @pytest.mark.parametrize("dense_min", ["1", "64", "256", "300"])
 @pytest.mark.parametrize("ht", ["", "1", "8"])
 def test_bsr16_hybrid_plan(monkeypatch, dense_min, ht):
