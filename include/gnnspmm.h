@@ -249,6 +249,15 @@ typedef struct {
     int32_t profile_reps;   /* timed runs per format for GS_SEL_PROFILE; 0 -> 3 */
     uint32_t formats;       /* candidates of MODEL and PROFILE: bit f set = gs_format f;
                                0 -> every format (the paper's whole pool) */
+    double mem_weight;      /* 1 - w of Eq. 1 (Sec. 4.3): the weight of the memory footprint against
+                               the running time, in [0, 1]; 0 -> time only (w = 1).  PROFILE picks
+                               the candidate with the smallest w R + (1 - w) M, R its measured time
+                               and M its device bytes, each min-max scaled over this (matrix, F)'s
+                               feasible candidates; O within 1e-4 of the smallest counts as tied
+                               (Fig. 6 caption) and the first in the order CSR, COO, ELL, DIA, BSR,
+                               CSC is taken.  MODEL needs a model trained for the same w (its "w" line, 1
+                               when absent): otherwise gs_ctx_create fails with GS_ERR_MODEL.  FIXED
+                               ignores it.  Outside [0, 1] or NaN: GS_ERR_INVALID_ARG. */
 } gs_selector_opts;
 
 int gs_ctx_create(const gs_selector_opts *o, gs_ctx *out);

@@ -64,7 +64,7 @@ class _Features(ctypes.Structure):
 class _SelOpts(ctypes.Structure):
     _fields_ = [("mode", _i32), ("fixed", _i32), ("model_path", ctypes.c_char_p),
                 ("max_bytes", _u64), ("bsr_block", _i32), ("profile_reps", _i32),
-                ("formats", ctypes.c_uint32)]
+                ("formats", ctypes.c_uint32), ("mem_weight", ctypes.c_double)]
 
 
 class _SelStats(ctypes.Structure):
@@ -373,11 +373,13 @@ class SelectContext:
 
     def __init__(self, mode: str = "model", fixed: str = "csr", model_path: str | None = None,
                  max_bytes: int | None = None, bsr_block: int = 16, profile_reps: int = 3,
-                 formats=None):
+                 formats=None, mem_weight: float = 0.0):
         """model_path None: the trained ensemble shipped in selector/model.gsm
         (the library's hand-set trees if that file is absent); "builtin": the
         hand-set trees.  formats: names of the candidate formats of "model"
-        and "profile" (None: all)."""
+        and "profile" (None: all).  mem_weight: 1 - w of Eq. 1, the weight of
+        the memory footprint against the running time (0: time only); "model"
+        needs a model trained for that w."""
         _require_gpu()
         if model_path is None:
             from paper_2111_00352_amd.selector import MODEL_PATH
@@ -388,7 +390,7 @@ class SelectContext:
         self._model_path = model_path.encode() if model_path else None
         mask = 0 if formats is None else sum(1 << FORMATS[f] for f in formats)
         o = _SelOpts(SEL_MODES[mode], FORMATS[fixed], self._model_path, int(max_bytes or 0),
-                     int(bsr_block), int(profile_reps), mask)
+                     int(bsr_block), int(profile_reps), mask, float(mem_weight))
         h = ctypes.c_void_p()
         _check(lib().gs_ctx_create(ctypes.byref(o), ctypes.byref(h)))
         self._h = h

@@ -37,6 +37,7 @@ struct Model {
     double mn[kNFeat] = {0}, mx[kNFeat] = {0};
     double base[GS_NUM_FORMATS] = {0};
     std::vector<Tree> trees;
+    double w = 1.0;  // the weight of Eq. 1 the model was trained for
 };
 
 

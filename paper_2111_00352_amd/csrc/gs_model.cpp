@@ -154,7 +154,8 @@ struct Tokens {
 // "tree cls nn" and nn nodes "feat thr left right value" (feat = -1 for a
 // leaf), numbers in decimal.  Version 2 is the same with every real written
 // as a hexadecimal literal and leaves as "L value", internal nodes as
-// "feat thr left right".
+// "feat thr left right".  Either may end with "w x": the weight of Eq. 1
+// whose labels the model learned (1 when absent).
 struct ModelError {
     std::string msg;
 };
@@ -223,6 +224,12 @@ void parse(const std::string &text, Model &m)
             if (n.feat >= 0 && (n.left <= i || n.right <= i || n.left >= nn || n.right >= nn))
                 bad("bad child index");
         }
+    }
+    const char *save = in.p;
+    if (in.is("w")) {
+        if (!real(m.w) || !(m.w >= 0.0 && m.w <= 1.0)) bad("w must be in [0, 1]");
+    } else {
+        in.p = save;
     }
 }
 

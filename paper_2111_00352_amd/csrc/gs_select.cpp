@@ -5,6 +5,7 @@
 // matrix is converted only when the chosen format has not been built for
 // this key yet, and the chosen format's kernel runs.
 
+#include <algorithm>
 #include <cctype>
 #include <cerrno>
 #include <chrono>
@@ -122,6 +123,32 @@ gs_matrix_ &ensure_built(gs_ctx_ &c, Entry &e, int fmt, hipStream_t s)
     return *e.built[fmt];
 }
 
+// Eq. 1 over the profiled candidates: the smallest w R + (1 - w) M, with
+// the running time R and the device bytes M min-max scaled over the
+// candidates; within 1e-4 of the smallest counts as optimal and the first in
+// tie order is taken.
+int eq1_choice(const Entry &e, uint32_t cand, double w)
+{
+    double tmin = 1e300, tmax = -1e300, mmin = 1e300, mmax = -1e300;
+    for (int fmt : kTieOrder)
+        if (cand & (1u << fmt)) {
+            tmin = std::min(tmin, e.prof_time[fmt]);
+            tmax = std::max(tmax, e.prof_time[fmt]);
+            mmin = std::min(mmin, (double)e.bytes[fmt]);
+            mmax = std::max(mmax, (double)e.bytes[fmt]);
+        }
+    auto scaled = [](double v, double lo, double hi) { return hi > lo ? (v - lo) / (hi - lo) : 0.0; };
+    double O[GS_NUM_FORMATS], best = 1e300;
+    for (int fmt : kTieOrder)
+        if (cand & (1u << fmt)) {
+            O[fmt] = w * scaled(e.prof_time[fmt], tmin, tmax) + (1.0 - w) * scaled((double)e.bytes[fmt], mmin, mmax);
+            best = std::min(best, O[fmt]);
+        }
+    for (int fmt : kTieOrder)
+        if ((cand & (1u << fmt)) && O[fmt] <= best + 1e-4) return fmt;
+    return GS_CSR;
+}
+
 int choose(gs_ctx_ &c, Entry &e, int64_t F, const float *X, int64_t ldx, float *Y, int64_t ldy,
            hipStream_t s)
 {
@@ -175,6 +202,7 @@ int choose(gs_ctx_ &c, Entry &e, int64_t F, const float *X, int64_t ldx, float *
             GS_HIP(hipEventCreate(&a));
             GS_HIP(hipEventCreate(&b));
             double best = 1e300;
+            uint32_t cand = 0;
             try {
                 for (int fmt : kTieOrder) {
                     if (!(e.feasible & c.opts.formats & (1u << fmt))) continue;
@@ -188,11 +216,13 @@ int choose(gs_ctx_ &c, Entry &e, int64_t F, const float *X, int64_t ldx, float *
                     GS_HIP(hipEventElapsedTime(&ms, a, b));
                     const double t = ms * 1e-3 / reps;
                     e.prof_time[fmt] = t;
+                    cand |= 1u << fmt;
                     if (t < best * 0.99) {  // within 1%: keep the earlier one in tie order
                         best = t;
                         chosen = fmt;
                     }
                 }
+                if (c.opts.mem_weight > 0.0 && cand) chosen = eq1_choice(e, cand, 1.0 - c.opts.mem_weight);
             } catch (...) {
                 (void)hipEventDestroy(a);
                 (void)hipEventDestroy(b);
@@ -221,7 +251,7 @@ int gs_ctx_create(const gs_selector_opts *o, gs_ctx *out)
     if (out) *out = nullptr;
     return guarded([&] {
         if (!out) fail(GS_ERR_INVALID_ARG, "null output handle");
-        gs_selector_opts r = {GS_SEL_MODEL, GS_CSR, nullptr, kDefaultMaxBytes, kDefaultBsrBlock, 3, 0};
+        gs_selector_opts r = {GS_SEL_MODEL, GS_CSR, nullptr, kDefaultMaxBytes, kDefaultBsrBlock, 3, 0, 0.0};
         if (o) r = *o;
         constexpr uint32_t kAll = (1u << GS_NUM_FORMATS) - 1;
         if (r.formats == 0) r.formats = kAll;
@@ -232,6 +262,8 @@ int gs_ctx_create(const gs_selector_opts *o, gs_ctx *out)
         if (r.bsr_block == 0) r.bsr_block = kDefaultBsrBlock;
         if (r.bsr_block < 1 || r.bsr_block > 64) fail(GS_ERR_INVALID_ARG, "bsr_block outside 1..64");
         if (r.profile_reps <= 0) r.profile_reps = 3;
+        if (!(r.mem_weight >= 0.0 && r.mem_weight <= 1.0))
+            fail(GS_ERR_INVALID_ARG, "mem_weight outside [0, 1]");
         gs_ctx_ *c = new gs_ctx_();
         try {
             c->opts = r;
@@ -251,6 +283,10 @@ int gs_ctx_create(const gs_selector_opts *o, gs_ctx *out)
                 }
                 std::string err;
                 if (!parse_model(text, c->model, &err)) fail(GS_ERR_MODEL, "%s", err.c_str());
+                // the model's labels fix its trade-off of Eq. 1
+                if (std::fabs((1.0 - r.mem_weight) - c->model.w) > 1e-9)
+                    fail(GS_ERR_MODEL, "the model was trained for w = %g, the context asks for w = %g",
+                         c->model.w, 1.0 - r.mem_weight);
             }
         } catch (...) {
             delete c;

@@ -1,6 +1,6 @@
 """Train the format predictor from profiled data and export it.
 
-Usage: python -m paper_2111_00352_amd.selector.train [DATA.csv] [--out model.gsm]
+Usage: python -m paper_2111_00352_amd.selector.train [DATA.csv] [--out model.gsm] [--w W]
            [--eval-csv eval.csv --eval-md generalisation.md] | [--importance importance.md] |
            [--w-sweep 0,0.25,... --md w_sweep.md]
 
@@ -83,7 +83,7 @@ def labels_eq1(T, M, w, tie=1e-4):
     """Eq. 1: the format minimising w R + (1 - w) M, with running time R and
     memory footprint M scaled to [0, 1] by the min and max over the whole
     profiled training set; formats within `tie` of the minimum count as
-    optimal (Fig. 5 caption) and the earliest in TIE_ORDER is taken."""
+    optimal (Fig. 6 caption) and the earliest in TIE_ORDER is taken."""
     ok = np.isfinite(T)
     tmin, tmax = T[ok].min(), T[ok].max()
     mmin, mmax = M[ok].min(), M[ok].max()
@@ -109,7 +109,7 @@ def fit(Xn, y, seed=0):
     return clf
 
 
-def export(clf, mn, mx, path):
+def export(clf, mn, mx, path, w=1.0):
     classes = list(clf.classes_)
     K = len(classes)
     lr = clf.learning_rate
@@ -146,6 +146,8 @@ def export(clf, mn, mx, path):
         lines.append(f"tree {cls} {len(nodes)}")
         for f, thr, l, r, v in nodes:
             lines.append(f"L {hx(v)}" if f < 0 else f"{f} {hx(thr)} {l} {r}")
+    if w != 1.0:  # the trade-off of Eq. 1 the labels were made for (1 when absent)
+        lines.append(f"w {hx(w)}")
     with open(path, "w") as fh:
         fh.write("\n".join(lines) + "\n")
     return trees, base_scores, classes
@@ -320,6 +322,9 @@ def main():
                                          "instead of exporting a model")
     ap.add_argument("--eval-csv", help="held-out profiles: evaluate the exported model on them")
     ap.add_argument("--eval-md", help="with --eval-csv: write the evaluation table (markdown)")
+    ap.add_argument("--w", type=float, default=1.0,
+                    help="weight of Eq. 1 for the exported model's labels (1: time only, with 3%% ties); "
+                         "a context uses it with mem_weight = 1 - w")
     a = ap.parse_args()
     from sklearn.model_selection import GroupKFold
 
@@ -328,7 +333,7 @@ def main():
         return w_sweep(a, X, T, groups, [float(v) for v in a.w_sweep.split(",")])
     if a.importance:
         return importance(a, X, T, groups)
-    y = labels(T)
+    y = labels(T) if a.w == 1.0 else labels_eq1(T, footprints(a.data), a.w)
     print(f"{len(y)} samples, {len(set(groups))} matrices; label counts: "
           + ", ".join(f"{TIE_ORDER[c]}={int((y == c).sum())}" for c in range(5)))
     # cross-validation on unseen matrices
@@ -350,7 +355,7 @@ def main():
     mn, mx = X.min(axis=0), X.max(axis=0)
     Xn = normalise(X, mn, mx)
     clf = fit(Xn, y)
-    trees, base, classes = export(clf, mn, mx, a.out)
+    trees, base, classes = export(clf, mn, mx, a.out, w=a.w)
     S = score_exported(trees, base, Xn)
     ours = np.array([classes[i] for i in np.argmax(S, axis=1)])
     agree = float((ours == clf.predict(Xn)).mean())

@@ -42,13 +42,16 @@ int main(int argc, char **argv)
     gs_matrix_info info;
     expect(gs_get_info(NULL, &info) == GS_ERR_INVALID_ARG, "info on a null handle");
 
-    gs_selector_opts so = {GS_SEL_MODEL, GS_CSR, NULL, 0, 16, 3, 1u << 9};
+    gs_selector_opts so = {GS_SEL_MODEL, GS_CSR, NULL, 0, 16, 3, 1u << 9, 0.0};
     gs_ctx ctx = NULL;
     expect(gs_ctx_create(&so, &ctx) == GS_ERR_INVALID_ARG && ctx == NULL, "candidate mask with an unknown format");
     so.formats = 0;
     so.mode = 7;
     expect(gs_ctx_create(&so, &ctx) == GS_ERR_INVALID_ARG, "unknown selector mode");
     so.mode = GS_SEL_PROFILE;
+    so.mem_weight = 1.5;
+    expect(gs_ctx_create(&so, &ctx) == GS_ERR_INVALID_ARG, "memory weight above 1");
+    so.mem_weight = 0.25;
     expect(gs_ctx_create(&so, &ctx) == GS_OK && ctx != NULL, "profiling context");
     gs_select_stats st;
     expect(gs_ctx_stats(ctx, &st) == GS_OK, "stats of a fresh context");
@@ -57,6 +60,8 @@ int main(int argc, char **argv)
         so.mode = GS_SEL_MODEL;
         so.model_path = argv[1];
         ctx = NULL;
+        expect(gs_ctx_create(&so, &ctx) == GS_ERR_MODEL && ctx == NULL, "model trained for another w");
+        so.mem_weight = 0.0;
         expect(gs_ctx_create(&so, &ctx) == GS_OK && ctx != NULL, "shipped model parses");
         gs_ctx_destroy(ctx);
     }

@@ -782,6 +782,47 @@ def test_select_and_run_modes(mode):
     assert oracle.check_spmm(_host(Y2), Yref2, M2)[0]
 
 
+def _footprints(f, b=16):
+    # device bytes of each candidate layout, the memory term M of Eq. 1
+    R, C, Z = f["n_rows"], f["n_cols"], f["nnz"]
+    return {"csr": 4 * (R + 1) + 8 * Z, "coo": 12 * Z, "ell": 8 * R * f["max_rd"],
+            "dia": 4 * f["n_diags"] * (R + 1), "bsr": 4 * (-(-R // b) + 1) + (12 + 4 * b * b) * f["n_blocks16"],
+            "csc": 4 * (C + 1) + 8 * Z}
+
+
+@pytest.mark.parametrize("kind", ["mesh", "uniform"])
+def test_profile_selection_trades_time_for_memory(kind):
+    # Eq. 1 in the exhaustive mode: with mem_weight 1 (w = 0) the smallest
+    # footprint wins (DIA on a stencil, ELL on rows of one length); with 0.5
+    # the chosen format's objective, from the measured times and the
+    # footprints, min-max scaled over the candidates, is within 1e-4 of the
+    # smallest.  The result is A.X either way.
+    if kind == "mesh":
+        g = graphgen.scaled(3)
+        case, X = _case_from_graph(g), g.X
+    else:
+        case = _uniform_long_rows(3000, 3000, 12, 12, 95)
+        X = graphgen.features_x(case.C, 64, 96, "normal")
+    shape = (case.R, case.C)
+    foot = _footprints(gs.extract_features(case.d_row, case.d_col, case.d_val, shape))
+    Yref, M = oracle.spmm(case.R, case.rp, case.ccol, case.cval, X)
+    order = ["csr", "coo", "ell", "dia", "bsr", "csc"]
+    for mw in (1.0, 0.5):
+        ctx = gs.SelectContext("profile", mem_weight=mw)
+        Y, fmt = ctx.run(3, case.d_row, case.d_col, case.d_val, shape, _dev(X))
+        assert oracle.check_spmm(_host(Y), Yref, M)[0]
+        st = ctx.stats()
+        cand = [f for f in order if st["feasible_mask"] & (1 << gs.FORMATS[f]) and st["scores"][f] > 0]
+        t = {f: st["scores"][f] for f in cand}
+        w = 1.0 - mw
+        sc = lambda v, d: (v - min(d.values())) / (max(d.values()) - min(d.values()))  # noqa: E731
+        O = {f: w * sc(t[f], t) + (1 - w) * sc(foot[f], {k: foot[k] for k in cand}) for f in cand}
+        assert O[fmt] <= min(O.values()) + 1e-4, (mw, fmt, O)
+        if mw == 1.0:
+            assert fmt == {"mesh": "dia", "uniform": "ell"}[kind]
+        ctx.close()
+
+
 def test_fixed_selector_reports_an_infeasible_format():
     # the fixed mode extracts no features; the build itself reports the cap
     g = graphgen.scaled(2)

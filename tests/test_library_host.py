@@ -61,7 +61,8 @@ def test_null_arguments_rejected_without_gpu(L):
 
 
 def _ctx(L, **kw):
-    o = gs._SelOpts(kw.get("mode", 0), kw.get("fixed", 1), kw.get("path"), 0, kw.get("b", 16), 3)
+    o = gs._SelOpts(kw.get("mode", 0), kw.get("fixed", 1), kw.get("path"), 0, kw.get("b", 16), 3, 0,
+                    kw.get("mem_weight", 0.0))
     h = ctypes.c_void_p()
     rc = L.gs_ctx_create(ctypes.byref(o), ctypes.byref(h))
     return rc, h
@@ -172,11 +173,33 @@ def test_trained_model_export_matches_sklearn(tmp_path):
     assert (np.array([classes[i] for i in S.argmax(axis=1)]) == clf.predict(Xn)).all()
 
 
+def test_memory_weight_of_eq1(L, tmp_path):
+    # mem_weight = 1 - w of Eq. 1: checked for [0, 1]; PROFILE takes any
+    # weight; MODEL only the w its model file was trained for ("w" line, 1
+    # when absent)
+    for bad in (-0.1, 1.5, float("nan")):
+        assert _ctx(L, mem_weight=bad)[0] == gs.ERR_INVALID_ARG
+    rc, h = _ctx(L, mode=1, mem_weight=0.7)
+    assert rc == 0
+    L.gs_ctx_destroy(h)
+    assert _ctx(L, mem_weight=0.5)[0] == gs.ERR_MODEL  # built-in model: w = 1
+    from paper_2111_00352_amd.selector import MODEL_PATH
+    text = open(MODEL_PATH).read()
+    for line, mw, want in (("w 0x1.0000000000000p-1", 0.5, 0), ("w 0x1.0000000000000p-1", 0.0, gs.ERR_MODEL),
+                           ("w 0x0.0p+0", 1.0, 0), ("w 0x1.8p+1", 0.0, gs.ERR_MODEL), ("w", 0.0, gs.ERR_MODEL)):
+        p = tmp_path / "w.gsm"
+        p.write_text(text + line + "\n")
+        rc, h = _ctx(L, path=str(p).encode(), mem_weight=mw)
+        assert rc == want, (line, mw)
+        if rc == 0:
+            L.gs_ctx_destroy(h)
+
+
 def test_candidate_mask_is_checked(L):
-    o = gs._SelOpts(0, 1, None, 0, 16, 3, 1 << 7)  # bit 7 names no format
+    o = gs._SelOpts(0, 1, None, 0, 16, 3, 1 << 7, 0.0)  # bit 7 names no format
     h = ctypes.c_void_p()
     assert L.gs_ctx_create(ctypes.byref(o), ctypes.byref(h)) == gs.ERR_INVALID_ARG
-    o = gs._SelOpts(0, 1, None, 0, 16, 3, (1 << 1) | (1 << 5))  # CSR and CSC only
+    o = gs._SelOpts(0, 1, None, 0, 16, 3, (1 << 1) | (1 << 5), 0.0)  # CSR and CSC only
     assert L.gs_ctx_create(ctypes.byref(o), ctypes.byref(h)) == 0
     L.gs_ctx_destroy(h)
 
