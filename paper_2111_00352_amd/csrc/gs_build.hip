@@ -982,6 +982,9 @@ gs_matrix_ *convert_from_csr(const gs_matrix_ &csr, int fmt, int bsr_block, uint
                 GS_LAUNCH_CHECK();
             }
             m->device_bytes = need;
+            // row tiles whose X window the SpMM may stage in LDS (rows of one chain only)
+            if (const char *e = std::getenv("GS_ELL_WINDOW"); Z > 0 && m->K <= kChainFold && !(e && std::string(e) == "off"))
+                count_windows(*m, rp, col, s);
             break;
         }
         case GS_DIA: {

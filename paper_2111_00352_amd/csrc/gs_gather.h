@@ -85,6 +85,51 @@ __device__ __forceinline__ void gather_batch(int cj, float vj, int j, int m,
 }
 
 
+// One batch of B entries j .. j+B-1 of the group's index batch in a row
+// tile whose X rows [w0, w1) are staged in LDS (xs, G*NQ float4 per row, the
+// lane's float4 at lane + G*q): in-window rows are read from LDS, the others
+// from global memory.  Slots past m gather a valid row and are dropped by a
+// select.
+template <int B, int NQ, int G>
+__device__ __forceinline__ void window_batch(int cj, float vj, int j, int m, const float4 *xs, int64_t w0,
+                                             int64_t w1, int lane, const float *__restrict__ X, int64_t ldx,
+                                             int64_t c0, const bool *qok, float *acc)
+{
+    constexpr int RW = G * NQ;
+    float4 x[B][NQ];
+    float v[B];
+#pragma unroll
+    for (int u = 0; u < B; u++) {
+        const int cu = __shfl(cj, j + u, G);
+        v[u] = __shfl(vj, j + u, G);
+        if (cu >= w0 && cu < w1) {
+            const float4 *xr = xs + (int64_t)(cu - w0) * RW + lane;
+#pragma unroll
+            for (int q = 0; q < NQ; q++) x[u][q] = xr[q * G];
+        } else {
+            const float *xp = X + (int64_t)cu * ldx + c0;
+#pragma unroll
+            for (int q = 0; q < NQ; q++)
+                x[u][q] = qok[q] ? load_x4(xp + 4 * G * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < B; u++) {
+        const bool live = j + u < m;
+#pragma unroll
+        for (int q = 0; q < NQ; q++) {
+            const float a0 = __builtin_fmaf(v[u], x[u][q].x, acc[4 * q + 0]);
+            const float a1 = __builtin_fmaf(v[u], x[u][q].y, acc[4 * q + 1]);
+            const float a2 = __builtin_fmaf(v[u], x[u][q].z, acc[4 * q + 2]);
+            const float a3 = __builtin_fmaf(v[u], x[u][q].w, acc[4 * q + 3]);
+            acc[4 * q + 0] = live ? a0 : acc[4 * q + 0];
+            acc[4 * q + 1] = live ? a1 : acc[4 * q + 1];
+            acc[4 * q + 2] = live ? a2 : acc[4 * q + 2];
+            acc[4 * q + 3] = live ? a3 : acc[4 * q + 3];
+        }
+    }
+}
+
 // Stores NQ float4 of acc to row pointer p (columns c0 + 4*G*q), streaming.
 template <int NQ, int G>
 __device__ __forceinline__ void store_row_stream(float *p, const bool *qok, const float *acc)

@@ -303,6 +303,15 @@ void spmm_csc(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t ldy,
 
 // Plans built at conversion time for the CSR and COO kernels.
 void plan_csr(gs_matrix_ &m, hipStream_t s);
+// Entries inside their row tile's window for every candidate tile (T = 32,
+// 64, 128, 256 rows, halo 0 / 1) of the matrix with CSR arrays rp, col, into
+// m.win_entries (synchronises s).
+void count_windows(gs_matrix_ &m, const int32_t *rp, const int32_t *col, hipStream_t s);
+// The LDS-staged row tile for m at row_bytes of X per staged row: the
+// counted candidate with the most in-window entries that fits the LDS budget,
+// when at least 65% of the entries are inside and the matrix has at least two
+// tiles per resident workgroup (false: no window).
+bool pick_window(const gs_matrix_ &m, int64_t row_bytes, int &T, int &h);
 void plan_coo(gs_matrix_ &m, const int32_t *row_ptr, hipStream_t s);
 
 // Vectorised CSR path; returns false when F / alignment do not allow it.

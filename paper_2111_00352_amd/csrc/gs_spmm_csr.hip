@@ -263,40 +263,8 @@ __global__ __launch_bounds__(kBlock) void k_csr_window(
                     cj = ld_stream(col + kb + lane);
                     vj = ld_stream(val + kb + lane);
                 }
-                for (int j = 0; j < m; j += B) {
-                    float4 x[B][NQ];
-                    float v[B];
-#pragma unroll
-                    for (int u = 0; u < B; u++) {
-                        const int cu = __shfl(cj, j + u, G);
-                        v[u] = __shfl(vj, j + u, G);
-                        if (cu >= w0 && cu < w1) {
-                            const float4 *xr = xs + (int64_t)(cu - w0) * RW + lane;
-#pragma unroll
-                            for (int q = 0; q < NQ; q++) x[u][q] = xr[q * G];
-                        } else {
-                            const float *xp = X + (int64_t)cu * ldx + c0;
-#pragma unroll
-                            for (int q = 0; q < NQ; q++)
-                                x[u][q] = qok[q] ? load_x4(xp + 4 * G * q) : make_float4(0.f, 0.f, 0.f, 0.f);
-                        }
-                    }
-#pragma unroll
-                    for (int u = 0; u < B; u++) {
-                        const bool live = j + u < m;
-#pragma unroll
-                        for (int q = 0; q < NQ; q++) {
-                            const float a0 = __builtin_fmaf(v[u], x[u][q].x, acc[4 * q + 0]);
-                            const float a1 = __builtin_fmaf(v[u], x[u][q].y, acc[4 * q + 1]);
-                            const float a2 = __builtin_fmaf(v[u], x[u][q].z, acc[4 * q + 2]);
-                            const float a3 = __builtin_fmaf(v[u], x[u][q].w, acc[4 * q + 3]);
-                            acc[4 * q + 0] = live ? a0 : acc[4 * q + 0];
-                            acc[4 * q + 1] = live ? a1 : acc[4 * q + 1];
-                            acc[4 * q + 2] = live ? a2 : acc[4 * q + 2];
-                            acc[4 * q + 3] = live ? a3 : acc[4 * q + 3];
-                        }
-                    }
-                }
+                for (int j = 0; j < m; j += B)
+                    window_batch<B, NQ, G>(cj, vj, j, m, xs, w0, w1, lane, X, ldx, c0, qok, acc);
             }
             store_row_stream<NQ, G>(Y + r * ldy + c0, qok, acc);
         }
@@ -551,21 +519,61 @@ __global__ __launch_bounds__(kBlock) void k_win_counts(const int32_t *__restrict
 // for each candidate tile and halo (read back), for the LDS-staged kernel.
 // Counted for natural-order matrices without long rows (GS_CSR_WINDOW = off
 // skips it).
-void plan_windows(gs_matrix_ &m, hipStream_t s)
+void count_windows(gs_matrix_ &m, const int32_t *rp, const int32_t *col, hipStream_t s)
 {
-    const char *e = std::getenv("GS_CSR_WINDOW");
-    if ((e && std::string(e) == "off") || m.csr_sorted || m.csr_grouped || m.n_long_rows > 0 || m.Z == 0) return;
     DevBuf cnt;
     cnt.alloc(sizeof(unsigned long long) * 2 * kWinCands, s);
     GS_HIP(hipMemsetAsync(cnt.p, 0, cnt.bytes, s));
-    k_win_counts<<<stats_grid(m.R), kBlock, 0, s>>>(m.row_ptr.as<int32_t>(), m.col.as<int32_t>(), m.R, m.C,
-                                                    cnt.as<unsigned long long>());
+    k_win_counts<<<stats_grid(m.R), kBlock, 0, s>>>(rp, col, m.R, m.C, cnt.as<unsigned long long>());
     GS_HIP(hipGetLastError());
     unsigned long long h[2 * kWinCands];
     GS_HIP(hipMemcpyAsync(h, cnt.p, sizeof h, hipMemcpyDeviceToHost, s));
     GS_HIP(hipStreamSynchronize(s));
     for (int i = 0; i < 2 * kWinCands; i++) m.win_entries[i] = (int64_t)h[i];
     m.win_counted = true;
+}
+
+void plan_windows(gs_matrix_ &m, hipStream_t s)
+{
+    const char *e = std::getenv("GS_CSR_WINDOW");
+    if ((e && std::string(e) == "off") || m.csr_sorted || m.csr_grouped || m.n_long_rows > 0 || m.Z == 0) return;
+    count_windows(m, m.row_ptr.as<int32_t>(), m.col.as<int32_t>(), s);
+}
+
+// Measured (F = 64..256): a tile pays for its staging only when most of its
+// entries are inside the window and there are several tiles per resident
+// workgroup.  On the mesh (about 60% inside) the staged ELL kernel took 38
+// against 34 us; on the block graph (76% inside, 6,400 tiles) 217 against
+// 236 us; on matrices of 10-15k rows (a few hundred tiles) the staged CSR and
+// ELL kernels were about twice as slow as the plain ones (stage, barrier and
+// rows in sequence on a short critical path).
+bool pick_window(const gs_matrix_ &m, int64_t row_bytes, int &T, int &h)
+{
+    T = h = 0;
+    if (!m.win_counted) return false;
+    const int64_t lds_cap = std::min<int64_t>(max_lds_bytes(), (int64_t)env_int("GS_CSR_WIN_KB", 32) * 1024);
+    const int64_t min_in = m.Z * env_int("GS_CSR_WIN_PCT", 65) / 100;
+    const int64_t min_tiles = env_int("GS_WIN_MIN_TILES", 2 * resident_workgroups());
+    int64_t best = -1;
+    for (int w = 0; w < kWinCands; w++)
+        for (int hh = 0; hh < 2; hh++) {
+            const int64_t bytes = (int64_t)((32 << w) + 2 * hh) * row_bytes;
+            const int64_t in = m.win_entries[2 * w + hh];
+            if (bytes <= lds_cap && in >= min_in && in > best && ceil_div(m.R, (int64_t)(32 << w)) >= min_tiles) {
+                best = in;
+                T = 32 << w;
+                h = hh;
+            }
+        }
+    if (const char *e = std::getenv("GS_CSR_WIN_T"); e && *e) {  // tests and sweeps: force a tile
+        const char *he = std::getenv("GS_CSR_WIN_H");
+        const int t = std::atoi(e), hh = he && std::atoi(he) > 0 ? 1 : 0;
+        if (t > 0 && (int64_t)(t + 2 * hh) * row_bytes <= max_lds_bytes()) {
+            T = t;
+            h = hh;
+        }
+    }
+    return T > 0;
 }
 
 // Reference classes of the columns, for gathers that keep often referenced X
@@ -761,36 +769,14 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
             }
         }
     }
-    // LDS-staged row tiles: the candidate (tile, halo) that keeps the most
-    // entries in the window within GS_CSR_WIN_KB (32 KiB) of LDS per
-    // workgroup, when at least half the entries are in it.  More LDS per
-    // workgroup costs resident waves: on the block-community graph (F = 256)
-    // tiles of 32 / 64 / 128 rows (32 / 64 / 128 KiB) measured 193 / 280 /
-    // 480 us against 209 us without staging.
+    // LDS-staged row tiles (pick_window): the candidate (tile, halo) that
+    // keeps the most entries in the window within GS_CSR_WIN_KB (32 KiB) of
+    // LDS per workgroup.  More LDS per workgroup costs resident waves: on the
+    // block-community graph (F = 256) tiles of 32 / 64 / 128 rows (32 / 64 /
+    // 128 KiB) measured 193 / 280 / 480 us against 209 us without staging
+    // (with today's plain kernel both take 203 us there).
     int win_T = 0, win_h = 0;
-    if (m.win_counted && m.n_long_rows == 0 && !m.csr_grouped) {
-        const int64_t lds_cap = std::min<int64_t>(max_lds_bytes(), (int64_t)env_int("GS_CSR_WIN_KB", 32) * 1024);
-        const int64_t min_in = m.Z * env_int("GS_CSR_WIN_PCT", 50) / 100;
-        int64_t best = -1;
-        for (int w = 0; w < kWinCands; w++)
-            for (int h = 0; h < 2; h++) {
-                const int64_t bytes = (int64_t)((32 << w) + 2 * h) * g * cpl * 4;
-                const int64_t in = m.win_entries[2 * w + h];
-                if (bytes <= lds_cap && in >= min_in && in > best) {
-                    best = in;
-                    win_T = 32 << w;
-                    win_h = h;
-                }
-            }
-        if (const char *e = std::getenv("GS_CSR_WIN_T"); e && *e) {  // tests and sweeps: force a tile
-            const char *hh = std::getenv("GS_CSR_WIN_H");
-            const int t = std::atoi(e), h = hh && std::atoi(hh) > 0 ? 1 : 0;
-            if (t > 0 && (int64_t)(t + 2 * h) * g * cpl * 4 <= max_lds_bytes()) {
-                win_T = t;
-                win_h = h;
-            }
-        }
-    }
+    if (m.n_long_rows == 0 && !m.csr_grouped) pick_window(m, (int64_t)g * cpl * 4, win_T, win_h);
     auto launch = [&](auto cpl_t, auto g_t, auto full_t) {
         constexpr int CPL = decltype(cpl_t)::value, G = decltype(g_t)::value;
         constexpr bool FU = decltype(full_t)::value;

@@ -100,6 +100,69 @@ __global__ __launch_bounds__(kBlock) void k_ell_fast(int64_t R, int64_t K,
     }
 }
 
+// ELL with the X rows of each row tile staged in LDS, for natural-order
+// matrices whose entries mostly stay near the diagonal (at most kChainFold
+// slots per row: one chain).  A workgroup takes T consecutive rows [r0, r1),
+// copies the X rows [r0 - halo, r1 + halo) of its column slice into LDS with
+// coalesced loads, and its groups run the rows as k_ell_fast does, reading
+// in-window columns from LDS and the others from global memory.
+template <int CPL, int G, bool FULL>
+__global__ __launch_bounds__(kBlock) void k_ell_window(int64_t R, int64_t C, int64_t K,
+                                                       const int32_t *__restrict__ ec,
+                                                       const float *__restrict__ ev,
+                                                       const float *__restrict__ X, int64_t ldx,
+                                                       float *__restrict__ Y, int64_t ldy, int64_t F, int T,
+                                                       int halo, int64_t ntiles)
+{
+    constexpr int GPB = kBlock / G;
+    constexpr int NQ = CPL / 4;
+    constexpr int RW = G * NQ;  // float4 per staged row
+    constexpr int B0 = 32 / CPL > 0 ? 32 / CPL : 1;
+    constexpr int B = B0 < G ? B0 : G;  // X rows in flight per batch
+    extern __shared__ float4 xs[];
+    const int g = threadIdx.x / G, lane = threadIdx.x % G;
+    const int gbase = (threadIdx.x % kWave) / G * G;
+    const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
+    const int64_t cbase = (int64_t)blockIdx.y * (G * CPL);
+    const int64_t c0 = cbase + (int64_t)lane * 4;
+    bool qok[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; q++) qok[q] = FULL || (c0 + 4 * G * q < F);
+
+    for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const int64_t r0 = t * T, r1 = r0 + T < R ? r0 + T : R;
+        const int64_t w0 = r0 - halo > 0 ? r0 - halo : 0;
+        const int64_t w1 = r1 + halo < C ? r1 + halo : C;
+        const int W = w1 > w0 ? (int)(w1 - w0) : 0;
+        __syncthreads();  // the previous tile's rows are done with xs
+        for (int idx = threadIdx.x; idx < W * RW; idx += kBlock) {
+            const int wr = idx / RW, j = idx - wr * RW;
+            const int64_t cc = cbase + 4 * j;
+            xs[idx] = (FULL || cc < F) ? load_x4(X + (w0 + wr) * ldx + cc) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        __syncthreads();
+        for (int64_t r = r0 + g; r < r1; r += GPB) {
+            float acc[CPL];
+#pragma unroll
+            for (int i = 0; i < CPL; i++) acc[i] = 0.0f;
+            for (int64_t kb = 0; kb < K; kb += G) {
+                int cj = -1;
+                float vj = 0.0f;
+                if (kb + lane < K) {
+                    cj = ld_stream(ec + (kb + lane) * R + r);
+                    vj = ld_stream(ev + (kb + lane) * R + r);
+                }
+                const int m = __popcll((__ballot(cj >= 0) >> gbase) & gmask);
+                if (cj < 0) cj = 0;  // padding lanes gather row 0 and are masked
+                for (int j = 0; j < m; j += B)
+                    window_batch<B, NQ, G>(cj, vj, j, m, xs, w0, w1, lane, X, ldx, c0, qok, acc);
+                if (m < G) break;
+            }
+            store_row_stream<NQ, G>(Y + r * ldy + c0, qok, acc);
+        }
+    }
+}
+
 // FOLD: more than kChainFold diagonals (the running sum of a row is added
 // into a total every kChainFold diagonals; compiled out otherwise).
 template <int CPL, int G, bool FULL, bool FOLD>
@@ -244,6 +307,17 @@ bool spmm_ell_fast(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
     return dispatch_fast(sh, [&](auto c_t, auto g_t, auto f_t) {
         constexpr int CPL = decltype(c_t)::value, G = decltype(g_t)::value;
         constexpr bool FU = decltype(f_t)::value;
+        int T = 0, h = 0;
+        if (m.K <= kChainFold && pick_window(m, (int64_t)G * CPL * 4, T, h)) {
+            const int64_t ntiles = ceil_div(m.R, T);
+            const size_t lds = (size_t)(T + 2 * h) * G * CPL * 4;
+            dim3 grid(persistent_grid(ntiles, sh.slices), (unsigned)sh.slices);
+            k_ell_window<CPL, G, FU><<<grid, kBlock, lds, s>>>(m.R, m.C, m.K, m.ell_col.as<int32_t>(),
+                                                              m.ell_val.as<float>(), X, ldx, Y, ldy, F, T, h,
+                                                              ntiles);
+            GS_HIP(hipGetLastError());
+            return;
+        }
         const int64_t tiles = ceil_div(m.R, kBlock / G);
         dim3 grid(persistent_grid(tiles, sh.slices), (unsigned)sh.slices);
         if (m.K > kChainFold)

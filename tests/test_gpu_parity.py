@@ -682,6 +682,28 @@ def test_csr_lds_window_tiles(monkeypatch, T, h):
         check_spmm(case, m, graphgen.features_x(C, 132, seed + 6, "normal"))
 
 
+@pytest.mark.parametrize("T,h", [("", ""), ("32", "0"), ("64", "1"), ("96", "0")])
+def test_ell_lds_window_tiles(monkeypatch, T, h):
+    # ELL rows of one tile with their X window staged in LDS (the tile the
+    # counts pick, or a forced one): communities, a stencil, ragged tiles,
+    # several column slices, strided operands, rectangular matrices
+    if T:
+        monkeypatch.setenv("GS_CSR_WIN_T", T)
+        monkeypatch.setenv("GS_CSR_WIN_H", h)
+    for k in (4, 3):
+        g = graphgen.scaled(k)
+        case = _case_from_graph(g)
+        m = check_layout(case, "ell")
+        check_spmm(case, m, g.X)
+        check_spmm(case, m, graphgen.features_x(case.C, 36, 180 + k, "normal"), ldx_pad=4, ldy_pad=8)
+        check_spmm(case, m, graphgen.features_x(case.C, 520, 190 + k, "normal"))
+    for R, C, seed in ((1003, 517, 181), (517, 1003, 182)):
+        case = _random_case(R, C, 9000, seed, empty=0.2)
+        m = case.build("ell")
+        check_spmm(case, m, graphgen.features_x(C, 64, seed + 5, "normal"))
+        check_spmm(case, m, graphgen.features_x(C, 132, seed + 6, "normal"))
+
+
 @pytest.mark.parametrize("P", [2, 5])
 def test_column_panel_schedule_sums_to_the_product(P):
     # the column-panel schedule that bench.py --column-panels measures: one
