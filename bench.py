@@ -115,7 +115,10 @@ def format_table(gs, row, col, val, shape, pairs, stream, reps, flops, balg):
         (d1,) = event_durations([lambda p: m.spmm(p[0], out=p[1])], stream, 1, pairs)
         n = adaptive_reps(float(d1[0]), reps)
         (d,) = event_durations([lambda p: m.spmm(p[0], out=p[1])], stream, n, pairs)
+        F = int(pairs[0][0].shape[1])
+        b_fmt = m.device_bytes + 4 * C * F + 4 * R * F  # the format's own A bytes + X + Y
         out[fmt] = {"feasible": True, **stats_row(d, flops, balg), "format_bytes": m.device_bytes,
+                    "b_fmt": b_fmt, "b_fmt_frac": round(b_fmt / float(np.median(d)) / 1e9 / HBM_PEAK_GBS, 4),
                     "build_s": round(t_build, 4)}
         m.close()
         del m
@@ -236,7 +239,7 @@ def other_workload(gs, k, dev, stream, reps):
     _, chosen = ctx.run(1, row, col, val, (R, C), pairs[0][0], out=pairs[0][1])
     torch.cuda.synchronize()
     ctx.close()
-    return {"workload": WORKLOADS[k], "n": R, "nnz": Z, "F": F, "B_alg": balg,
+    return {"workload": WORKLOADS[k], "n": R, "nnz": Z, "F": F, "B_alg": balg, "gather_bytes_no_reuse": 4 * Z * F,
             "selector": selector_summary(fmts, chosen), "formats": fmts}
 
 
@@ -545,6 +548,7 @@ def main():
             "traffic_unit": "MB per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "traffic_rate_gbs": None if traffic is None else round(traffic * 1e6 / (dom["mean_us"] * 1e-6) / 1e9, 1),
             "bytes_per_launch": balg1,
+            "gather_bytes_no_reuse": 4 * Z * F,
             "launch_us": dom["mean_us"],
             "layers": layers,
         },
