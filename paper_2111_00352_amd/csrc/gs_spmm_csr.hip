@@ -444,45 +444,94 @@ __device__ __forceinline__ int col_class(int n)
     return b < 15 ? b : 15;
 }
 
-// Columns per reference class (16 bins, added into hist).
-__global__ __launch_bounds__(kBlock) void k_class_hist(const int32_t *__restrict__ cc, int64_t C,
-                                                       int32_t *__restrict__ hist)
+// Reference class of every column, one byte each (so that the tagging pass
+// gathers from an array a quarter the size of the counts), and the number of
+// columns per class.  The 16 bins are counted per wave by ballots (a power
+// law puts most columns in two classes: LDS atomics on one bin serialised),
+// and each workgroup writes its own 16 counts to part (atomics of thousands
+// of workgroups on the same 16 words queued: 50 us at 2M columns);
+// k_class_total adds them.
+__global__ __launch_bounds__(kBlock) void k_col_classes(const int32_t *__restrict__ cc, int64_t C,
+                                                        uint8_t *__restrict__ cls, int32_t *__restrict__ part)
+{
+    constexpr int U = 4;  // columns per lane in flight
+    __shared__ int h[16];
+    if (threadIdx.x < 16) h[threadIdx.x] = 0;
+    __syncthreads();
+    const int lane = threadIdx.x % kWave;
+    const int64_t stride = (int64_t)gridDim.x * kBlock * U;
+    // every lane of a wave runs the same number of rounds, so the ballots see whole waves
+    for (int64_t j0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x - lane) * U; j0 < C; j0 += stride) {
+        int k[U];
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int64_t j = j0 + u * kWave + lane;
+            k[u] = j < C ? cc[j] : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int64_t j = j0 + u * kWave + lane;
+            if (k[u] >= 0) {
+                k[u] = col_class(k[u]);
+                cls[j] = (uint8_t)k[u];
+            }
+        }
+        for (int c = 0; c < 16; c++) {
+            int n = 0;
+#pragma unroll
+            for (int u = 0; u < U; u++) n += __popcll(__ballot(k[u] == c));
+            if (lane == 0 && n) atomicAdd(&h[c], n);
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < 16) part[(int64_t)blockIdx.x * 16 + threadIdx.x] = h[threadIdx.x];
+}
+
+// hist[c] = the sum of the G workgroups' counts of class c (one workgroup;
+// sixteen readers per class, each adding every sixteenth workgroup's count).
+__global__ __launch_bounds__(kBlock) void k_class_total(const int32_t *__restrict__ part, int G,
+                                                        int32_t *__restrict__ hist)
 {
     __shared__ int h[16];
     if (threadIdx.x < 16) h[threadIdx.x] = 0;
     __syncthreads();
-    for (int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x; j < C; j += (int64_t)gridDim.x * kBlock)
-        atomicAdd(&h[col_class(cc[j])], 1);
+    const int c = threadIdx.x % 16;
+    int sum = 0;
+    for (int i = threadIdx.x / 16; i < G; i += kBlock / 16) sum += part[(int64_t)i * 16 + c];
+    atomicAdd(&h[c], sum);
     __syncthreads();
-    if (threadIdx.x < 16 && h[threadIdx.x]) atomicAdd(&hist[threadIdx.x], h[threadIdx.x]);
+    if (threadIdx.x < 16) hist[threadIdx.x] = h[threadIdx.x];
 }
 
-// Reference class of every column, one byte each (so that the tagging pass
-// gathers from an array a quarter the size of the counts).
-__global__ __launch_bounds__(kBlock) void k_col_classes(const int32_t *__restrict__ cc, int64_t C,
-                                                        uint8_t *__restrict__ cls)
-{
-    for (int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x; j < C; j += (int64_t)gridDim.x * kBlock)
-        cls[j] = (uint8_t)col_class(cc[j]);
-}
-
-// Class-tagged copy of the column indices: col | class(col) << 27, four
-// entries per thread.
+// Class-tagged copy of the column indices: col | class(col) << 27.  Sixteen
+// entries per thread (four 16-byte loads and stores), so that sixteen class
+// bytes are gathered at once; a scalar tail.
 __global__ __launch_bounds__(kBlock) void k_tag_cols(const int32_t *__restrict__ col, int64_t Z,
                                                      const uint8_t *__restrict__ cls, int32_t *__restrict__ tagged)
 {
-    for (int64_t e0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * 4; e0 < Z;
-         e0 += (int64_t)gridDim.x * kBlock * 4) {
-        int c[4];
+    const int64_t nv = Z / 16;  // whole groups of sixteen
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t v = (int64_t)blockIdx.x * kBlock + threadIdx.x; v < nv; v += stride) {
+        const int4 *src = reinterpret_cast<const int4 *>(col) + v * 4;
+        int4 c[4];
 #pragma unroll
-        for (int u = 0; u < 4; u++) c[u] = e0 + u < Z ? col[e0 + u] : 0;
-        int t[4];
+        for (int u = 0; u < 4; u++) c[u] = src[u];
+        int t[16];
 #pragma unroll
-        for (int u = 0; u < 4; u++) t[u] = (int)cls[c[u]];
+        for (int u = 0; u < 4; u++) {
+            t[4 * u + 0] = cls[c[u].x];
+            t[4 * u + 1] = cls[c[u].y];
+            t[4 * u + 2] = cls[c[u].z];
+            t[4 * u + 3] = cls[c[u].w];
+        }
+        int4 *dst = reinterpret_cast<int4 *>(tagged) + v * 4;
 #pragma unroll
         for (int u = 0; u < 4; u++)
-            if (e0 + u < Z) tagged[e0 + u] = c[u] | (t[u] << kColClassShift);
+            dst[u] = make_int4(c[u].x | (t[4 * u + 0] << kColClassShift), c[u].y | (t[4 * u + 1] << kColClassShift),
+                               c[u].z | (t[4 * u + 2] << kColClassShift), c[u].w | (t[4 * u + 3] << kColClassShift));
     }
+    for (int64_t e = nv * 16 + (int64_t)blockIdx.x * kBlock + threadIdx.x; e < Z; e += stride)
+        tagged[e] = col[e] | ((int)cls[col[e]] << kColClassShift);
 }
 
 // Entries whose column lies in their row's tile window, for the row tiles
@@ -595,12 +644,14 @@ void plan_col_classes(gs_matrix_ &m, hipStream_t s)
         cc.alloc((size_t)m.C * 4, s);
         column_counts(m.col.as<int32_t>(), m.C, m.Z, cc.as<int32_t>(), s);
     }
+    const unsigned G = std::min(plan_grid(ceil_div(m.C, 4)), 512u);
+    DevBuf part;
+    part.alloc((size_t)G * 16 * 4, s);
     hist.alloc(16 * 4, s);
-    GS_HIP(hipMemsetAsync(hist.p, 0, 16 * 4, s));
-    k_class_hist<<<plan_grid(m.C), kBlock, 0, s>>>(cc.as<int32_t>(), m.C, hist.as<int32_t>());
-    GS_HIP(hipGetLastError());
     m.col_cls.alloc((size_t)m.C, s);
-    k_col_classes<<<plan_grid(m.C), kBlock, 0, s>>>(cc.as<int32_t>(), m.C, m.col_cls.as<uint8_t>());
+    k_col_classes<<<G, kBlock, 0, s>>>(cc.as<int32_t>(), m.C, m.col_cls.as<uint8_t>(), part.as<int32_t>());
+    GS_HIP(hipGetLastError());
+    k_class_total<<<1, kBlock, 0, s>>>(part.as<int32_t>(), (int)G, hist.as<int32_t>());
     GS_HIP(hipGetLastError());
     int32_t h[16];
     GS_HIP(hipMemcpyAsync(h, hist.p, sizeof h, hipMemcpyDeviceToHost, s));
@@ -763,7 +814,7 @@ bool spmm_csr_vec4(gs_matrix_ &m, const float *X, int64_t ldx, float *Y, int64_t
                 hot_cls = 0;  // no allocation allowed: plain gathers
             } else {          // first use: the class-tagged column copy
                 m.csr_colf.alloc((size_t)m.Z * 4, s);
-                k_tag_cols<<<plan_grid(ceil_div(m.Z, 4)), kBlock, 0, s>>>(
+                k_tag_cols<<<plan_grid(ceil_div(m.Z, 16)), kBlock, 0, s>>>(
                     m.col.as<int32_t>(), m.Z, m.col_cls.as<uint8_t>(), m.csr_colf.as<int32_t>());
                 GS_HIP(hipGetLastError());
             }
