@@ -452,8 +452,12 @@ __global__ __launch_bounds__(kTB) void k_bsr_count(const int32_t *__restrict__ r
 
 // Block count with a bitmap of block columns in LDS (nbc bits), one
 // workgroup per block row (persistent): the block row's entries are one
-// contiguous range of col[], each marks its block column, the count is the
-// bitmap's population.
+// contiguous range of col[], each sets its block column's bit, and the
+// entries that found their bit clear count the distinct blocks.  The bitmap
+// is zero at the top of every block row: after the count the touched words
+// are cleared again by re-reading the entries when they are fewer than the
+// bitmap's words (wide matrices: the whole-bitmap clear and population count
+// had cost 267 us at 2M columns), the whole bitmap otherwise.
 __global__ __launch_bounds__(kTB) void k_bsr_count_lds(const int32_t *__restrict__ rp,
                                                        const int32_t *__restrict__ col, int64_t R,
                                                        int b, int64_t nbr, int64_t nw,
@@ -461,27 +465,30 @@ __global__ __launch_bounds__(kTB) void k_bsr_count_lds(const int32_t *__restrict
 {
     extern __shared__ uint32_t bmp[];
     __shared__ int wsum[kTB / kWave];
+    for (int64_t w = threadIdx.x; w < nw; w += kTB) bmp[w] = 0u;
+    __syncthreads();
     for (int64_t br = blockIdx.x; br < nbr; br += gridDim.x) {
-        for (int64_t w = threadIdx.x; w < nw; w += kTB) bmp[w] = 0u;
-        __syncthreads();
         const int64_t r1 = (br + 1) * b < R ? (br + 1) * b : R;
         const int64_t k0 = rp[br * b], k1 = rp[r1];
-        for (int64_t kk = k0 + threadIdx.x; kk < k1; kk += kTB) {
-            const uint32_t c = (uint32_t)(col[kk] / b);
-            atomicOr(&bmp[c >> 5], 1u << (c & 31));
-        }
-        __syncthreads();
         int n = 0;
-        for (int64_t w = threadIdx.x; w < nw; w += kTB) n += __popc(bmp[w]);
+        for (int64_t kk = k0 + threadIdx.x; kk < k1; kk += kTB) {
+            const uint32_t c = (uint32_t)(col[kk] / b), bit = 1u << (c & 31);
+            n += (atomicOr(&bmp[c >> 5], bit) & bit) ? 0 : 1;
+        }
         n = wave_sum_i32(n);
         if (lane_id() == 0) wsum[threadIdx.x / kWave] = n;
-        __syncthreads();
+        __syncthreads();  // every bit of this block row is set and counted
+        if (k1 - k0 < nw) {
+            for (int64_t kk = k0 + threadIdx.x; kk < k1; kk += kTB) bmp[(uint32_t)(col[kk] / b) >> 5] = 0u;
+        } else {
+            for (int64_t w = threadIdx.x; w < nw; w += kTB) bmp[w] = 0u;
+        }
         if (threadIdx.x == 0) {
             int t = 0;
             for (int i = 0; i < kTB / kWave; i++) t += wsum[i];
             cnt[br] = t;
         }
-        __syncthreads();
+        __syncthreads();  // the bitmap is clear and wsum read before the next block row
     }
 }
 
