@@ -471,9 +471,16 @@ __global__ __launch_bounds__(kTB) void k_bsr_count_lds(const int32_t *__restrict
         const int64_t r1 = (br + 1) * b < R ? (br + 1) * b : R;
         const int64_t k0 = rp[br * b], k1 = rp[r1];
         int n = 0;
-        for (int64_t kk = k0 + threadIdx.x; kk < k1; kk += kTB) {
-            const uint32_t c = (uint32_t)(col[kk] / b), bit = 1u << (c & 31);
-            n += (atomicOr(&bmp[c >> 5], bit) & bit) ? 0 : 1;
+        constexpr int U = 4;  // column loads in flight per thread (clamped indices: no branch per load)
+        for (int64_t kb = k0 + threadIdx.x; kb < k1; kb += U * kTB) {
+            int cv[U];
+#pragma unroll
+            for (int u = 0; u < U; u++) cv[u] = col[kb + u * kTB < k1 ? kb + u * kTB : k1 - 1];
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const uint32_t c = (uint32_t)(cv[u] / b), bit = 1u << (c & 31);
+                if (kb + u * kTB < k1) n += (atomicOr(&bmp[c >> 5], bit) & bit) ? 0 : 1;
+            }
         }
         n = wave_sum_i32(n);
         if (lane_id() == 0) wsum[threadIdx.x / kWave] = n;
