@@ -165,10 +165,10 @@ int gs_spmm(gs_matrix A, const float *X, int64_t ldx, float *Y, int64_t ldy, int
  * Supported for CSR, ELL, DIA, BSR and CSC handles built by gs_build_format
  * or gs_convert.  Errors: GS_ERR_UNSUPPORTED for a COO handle (its range
  * tables are built, and allocated, per launch shape on first use) and when
- * the workspace would exceed GS_NOALLOC_SCRATCH_BYTES (CSR: 4 * F bytes per
- * 128-entry chunk of rows longer than 1,024 entries, or longer than 128 when
- * F is not a multiple of 4 or an operand is not 16-byte aligned; CSC:
- * 8 * n_rows * F bytes); otherwise as gs_spmm.  Asynchronous on s. */
+ * the workspace would exceed GS_NOALLOC_SCRATCH_BYTES (CSR: at most 4 * F
+ * bytes per 128 entries of the rows longer than 128 entries, as many as the
+ * row plan cuts into chunks; CSC: 8 * n_rows * F bytes); otherwise as
+ * gs_spmm.  Asynchronous on s. */
 #define GS_NOALLOC_SCRATCH_BYTES (64u << 20)
 int gs_spmm_noalloc(gs_matrix A, const float *X, int64_t ldx, float *Y, int64_t ldy, int64_t F,
                     gs_stream s);

@@ -974,3 +974,8 @@ def test_block_count_kernels_agree(monkeypatch, merge):
     check_features(case)
     for b in (3, 16, 64):
         check_layout(case, "bsr", b)
+    # wide and sparse: block rows hold fewer entries than the bitmap has
+    # words, so the count clears only the words its entries touched
+    case = _random_case(300, 200003, 3000, 72, empty=0.3)
+    check_features(case)
+    check_layout(case, "bsr", 16)
