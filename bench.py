@@ -66,6 +66,21 @@ def b_alg(R, C, Z, F):
     return 4 * (R + 1) + 8 * Z + 4 * C * F + 4 * R * F
 
 
+def profiled_traffic(workload: str, fmt: str, root: str = ROOT):
+    """HBM traffic per SpMM (MB, FETCH_SIZE + WRITE_SIZE, copy-calibrated)
+    of `fmt` on `workload` from profiles/traffic_<workload>_<fmt>.json, or
+    None when there is no such file or it was measured on other device
+    sources than the ones present (their hash differs)."""
+    tpath = os.path.join(root, "profiles", f"traffic_{workload}_{fmt}.json")
+    if not os.path.exists(tpath):
+        return None
+    from paper_2111_00352_amd.profsum import source_hash
+
+    with open(tpath) as f:
+        tj = json.load(f)
+    return round(tj["bytes"] / 1e6, 2) if tj.get("source_hash") == source_hash() else None
+
+
 def event_durations(fns, stream, reps, inputs):
     """Per-call durations (s) of each fn in fns, called in turn reps times on
     rotating inputs and bracketed by HIP events recorded on `stream` (the
@@ -512,15 +527,7 @@ def main():
     # the same matrix and width); the time is the mean launch duration
     dom = layers[0]
     achieved = dom["achieved_gbs"]
-    traffic = None
-    tpath = os.path.join(ROOT, "profiles", f"traffic_{WORKLOAD_KEYS[k]}_{chosen1}.json")
-    if os.path.exists(tpath):
-        from paper_2111_00352_amd.profsum import source_hash
-
-        with open(tpath) as f:
-            tj = json.load(f)
-        if tj.get("source_hash") == source_hash():
-            traffic = round(tj["bytes"] / 1e6, 2)
+    traffic = profiled_traffic(WORKLOAD_KEYS[k], chosen1)
 
     out = {
         "metric": METRIC,
