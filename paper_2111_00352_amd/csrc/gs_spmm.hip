@@ -573,10 +573,23 @@ __global__ __launch_bounds__(kBlock) void k_csc_scatter(int64_t C, const int32_t
     for (int64_t j = ((int64_t)blockIdx.x * kBlock + threadIdx.x) / kWave; j < C; j += waves) {
         const int32_t k0 = cp[j], k1 = cp[j + 1];
         if (k0 == k1) continue;
-        for (int64_t c = lane; c < F; c += kWave) {
-            const double x = (double)X[j * ldx + c];
-            for (int32_t k = k0; k < k1; k++)
-                unsafeAtomicAdd(&W[(int64_t)ri[k] * F + c], (double)val[k] * x);
+        for (int64_t c0 = 0; c0 < F; c0 += 2 * kWave) {  // two X values per lane
+            const int64_t ca = c0 + lane, cb = c0 + kWave + lane;
+            const double xa = ca < F ? (double)X[j * ldx + ca] : 0.0;
+            const double xb = cb < F ? (double)X[j * ldx + cb] : 0.0;
+            // the column's entries 64 at a time: one row index and value per
+            // lane, broadcast to the wave by shuffles
+            for (int32_t kb = k0; kb < k1; kb += kWave) {
+                const int n = k1 - kb < kWave ? k1 - kb : kWave;
+                const int32_t rl = lane < n ? ri[kb + lane] : 0;
+                const float vl = lane < n ? val[kb + lane] : 0.0f;
+                for (int u = 0; u < n; u++) {
+                    const int64_t r = __shfl(rl, u);
+                    const double v = (double)__shfl(vl, u);
+                    if (ca < F) unsafeAtomicAdd(&W[r * F + ca], v * xa);
+                    if (cb < F) unsafeAtomicAdd(&W[r * F + cb], v * xb);
+                }
+            }
         }
     }
 }
