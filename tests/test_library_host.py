@@ -173,6 +173,24 @@ def test_trained_model_export_matches_sklearn(tmp_path):
     assert (np.array([classes[i] for i in S.argmax(axis=1)]) == clf.predict(Xn)).all()
 
 
+def test_model_trained_for_a_weight_of_eq1(L, tmp_path):
+    # a model trained on Eq. 1 labels for w = 0.25 records its w; a context
+    # accepts it only with mem_weight = 0.75
+    from paper_2111_00352_amd.selector import DATA_PATH, train
+    X, T, _, _ = train.load(DATA_PATH)
+    y = train.labels_eq1(T, train.footprints(DATA_PATH), 0.25)
+    mn, mx = X.min(axis=0), X.max(axis=0)
+    clf = train.fit(train.normalise(X, mn, mx), y)
+    path = tmp_path / "w.gsm"
+    train.export(clf, mn, mx, str(path), w=0.25)
+    assert open(path).read().splitlines()[-1] == "w " + (0.25).hex()
+    for mw, want in ((0.75, 0), (0.0, gs.ERR_MODEL), (0.5, gs.ERR_MODEL)):
+        rc, h = _ctx(L, path=str(path).encode(), mem_weight=mw)
+        assert rc == want, mw
+        if rc == 0:
+            L.gs_ctx_destroy(h)
+
+
 def test_memory_weight_of_eq1(L, tmp_path):
     # mem_weight = 1 - w of Eq. 1: checked for [0, 1]; PROFILE takes any
     # weight; MODEL only the w its model file was trained for ("w" line, 1
