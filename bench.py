@@ -300,6 +300,47 @@ def gather_ceiling(gs, dev, stream, reps=10):
     return {"rows": R, "entries_per_row": d, "F": F, "table": rows}
 
 
+def x_footprint_floor(gs, g, dev, stream, reps=10):
+    """The workload's own row structure against smaller X: every column
+    index is folded into the first n_x columns (col mod n_x; entries that
+    then repeat in a row are dropped), for X footprints that fit one XCD's L2
+    (4 MiB) and the memory-side cache (64 MiB), beside the real one.  The
+    SpMM time with X in L2 is the floor set by the rows' work itself; the gap
+    to the real time is what the memory system adds for the gathers."""
+    import torch
+
+    R, C, F = g.R, g.C, g.F
+    row = torch.from_numpy(g.row).to(dev).to(torch.int64)
+    col = torch.from_numpy(g.col).to(dev).to(torch.int64)
+    val = torch.from_numpy(g.val).to(dev)
+    out = []
+    for mib in (4, 64, None):
+        n_x = C if mib is None else min(C, mib * 2**20 // (F * 4))
+        c2 = col % n_x
+        key = row * n_x + c2
+        uk, first = torch.unique(key, sorted=True, return_inverse=True)
+        # keep the first entry of every (row, folded column): a scatter of indices
+        idx = torch.full((uk.numel(),), key.numel(), dtype=torch.int64, device=dev)
+        idx.scatter_reduce_(0, first, torch.arange(key.numel(), device=dev), reduce="amin")
+        r2, cc2, v2 = (uk // n_x).to(torch.int32), (uk % n_x).to(torch.int32), val[idx]
+        m = gs.build_format(r2, cc2, v2, (R, n_x), "csr")
+        X = torch.randn((n_x, F), device=dev)
+        Ys = [torch.empty((R, F), device=dev) for _ in range(2)]
+        pairs = [(X, y) for y in Ys]
+        for i in range(3):
+            m.spmm(X, out=Ys[i % 2])
+        (d,) = event_durations([lambda p: m.spmm(p[0], out=p[1])], stream, reps, pairs)
+        t = float(np.median(d))
+        Z2 = int(uk.numel())
+        out.append({"x_mib": round(n_x * F * 4 / 2**20, 1), "n_cols": n_x, "nnz": Z2,
+                    "median_us": round(t * 1e6, 1), "requested_gather_gbs": round(Z2 * F * 4 / t / 1e9, 1)})
+        log(f"X footprint {out[-1]['x_mib']} MiB: {out[-1]}")
+        m.close()
+        del m, X, Ys, pairs, uk, first, idx, r2, cc2, v2, key, c2
+        torch.cuda.empty_cache()
+    return {"n": R, "F": F, "table": out}
+
+
 def column_panels(gs, g, dev, stream, parts, reps=10):
     """Column-panel (2-D) schedule of the CSR SpMM: A's columns are cut into
     P equal ranges, one CSR handle per panel, and the panels run one after
@@ -372,6 +413,8 @@ def main():
     ap.add_argument("--gcn-epochs", type=int, default=10)
     ap.add_argument("--gather-ceiling", action="store_true",
                     help="only the random-gather ceiling table of the CSR kernel (X of 2 MiB .. 1 GiB)")
+    ap.add_argument("--x-floor", action="store_true",
+                    help="only the X-footprint table of --config's row structure (X folded to 4 MiB, 64 MiB, real)")
     ap.add_argument("--column-panels", default=None,
                     help="only the column-panel schedule table of the CSR SpMM on --config: "
                          "comma-separated panel counts, e.g. 1,2,4,8,16")
@@ -401,6 +444,11 @@ def main():
         return
     k = args.config
     two_layer = k == 5
+    if args.x_floor:
+        res = x_footprint_floor(gs, graphgen.config(k), dev, stream, reps=max(args.format_reps // 2, 10))
+        res["workload"] = WORKLOADS[k]
+        print(json.dumps({"x_footprint_floor": res}), flush=True)
+        return
     if args.column_panels:
         g = graphgen.config(k)
         parts = [int(x) for x in args.column_panels.split(",") if x]
